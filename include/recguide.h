@@ -1,0 +1,196 @@
+/*
+ * recguide.h -- C ABI of the MI355X (gfx950) draft-verify hot path of
+ * RecGuide (Reciprocal Guidance for diffusion-AR self-speculation).
+ *
+ * One fused forward step of a shared-backbone self-speculation model runs,
+ * per request, the verify rows of the previous draft block and the rows of
+ * the next draft block in the same batch.  This library provides the three
+ * data-parallel pieces of that step:
+ *
+ *   rg_draft_verify_attention  attention of those rows over a paged KV cache
+ *                              with the hybrid mask of Eq. 1 (Sec. 3.1)
+ *   rg_verify_accept           verifier argmax / entropy per row and greedy
+ *                              first-mismatch acceptance per request
+ *                              (Sec. 3.1; e_t of Sec. 5.2)
+ *   rg_draft_confidence        draft confidence P_1st, top-2 margin
+ *                              P_1st - P_2nd and entropy per draft row
+ *                              (Sec. 4.1)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - bf16 tensors are passed as their raw 16-bit patterns (uint16_t).
+ * - Pointers documented as "device" must point to memory the GPU can read
+ *   or write (hipMalloc / torch CUDA tensors); "host" pointers are read by
+ *   the CPU during the call only and may be reused as soon as it returns.
+ * - The caller owns every buffer, including the workspace.  The library
+ *   allocates no device memory and keeps no mutable global state; calls on
+ *   different streams are independent provided they use distinct workspaces
+ *   and outputs.
+ * - Every call validates its arguments on the host first.  On a validation
+ *   error it returns the error code, enqueues nothing and leaves every output
+ *   untouched.  Otherwise it enqueues its kernels on `stream` (a hipStream_t,
+ *   NULL = the default stream) and returns without synchronising; outputs are
+ *   valid once the stream reaches that point.  A failed launch returns
+ *   RG_ERR_HIP.
+ * - Workspaces: size them with the matching *_workspace query (same
+ *   arguments).  The logit entry points keep completion counters in their
+ *   workspace: it must hold zeros before its first use (a zero-filled
+ *   allocation, or rg_workspace_zero), and every completed call leaves those
+ *   counters at zero again, so it can be reused without clearing.  Two calls
+ *   in flight at once must not share a workspace.
+ * - Inputs must be finite.
+ */
+#ifndef RECGUIDE_H
+#define RECGUIDE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RG_ABI_VERSION 1
+
+typedef int32_t rg_status;
+#define RG_OK 0
+#define RG_ERR_NULL 1        /* a required pointer is NULL                     */
+#define RG_ERR_SHAPE 2       /* sizes or offsets are inconsistent             */
+#define RG_ERR_UNSUPPORTED 3 /* valid but not supported (head_dim, page size) */
+#define RG_ERR_WORKSPACE 4   /* workspace NULL or smaller than required       */
+#define RG_ERR_HIP 5         /* a HIP launch or runtime call failed           */
+
+/* Version of this ABI (RG_ABI_VERSION of the built library). */
+int32_t rg_abi_version(void);
+
+/* Static description of a status code. */
+const char* rg_status_string(rg_status status);
+
+/* Largest number of requests planned into one attention launch; larger
+ * batches are split into several launches by the library itself. */
+#define RG_ATTN_MAX_REQS_PER_LAUNCH 128
+
+/*
+ * Ragged batch layout of one fused draft-verify step (attention).
+ *
+ * Request r has ctx_len[r] = L tokens already in its pages and
+ * n_r = q_indptr[r+1] - q_indptr[r] new query rows: first n_verify[r] = V
+ * verify rows (the previous draft block), then B = n_r - V rows of the next
+ * draft block.  The K/V of all n_r new rows must already be written to the
+ * request's pages, so its keys are positions 0 .. T-1 with T = L + n_r.
+ *
+ * Mask (Eq. 1 with prefix = context + verify rows, draft set = next block):
+ * verify row i (0 <= i < V) sees keys j <= L + i; draft rows see all T keys.
+ *
+ * Paged cache, page size 16 tokens.  Token j of request r lives in slot
+ * j % 16 of page page_indices[page_indptr[r] + j / 16]; the request must own
+ * at least ceil(T / 16) pages.  Cache layouts (contiguous):
+ *   k_cache [num_pages][num_kv_heads][16][head_dim]   token-major pages
+ *   v_cache [num_pages][num_kv_heads][head_dim][16]   dimension-major pages
+ * Slots and pages no request reads may hold anything, NaN included.
+ *
+ * Grouped-query attention: query head h reads KV head h / (Hq / Hkv).
+ */
+typedef struct rg_attn_layout {
+  int32_t num_requests;   /* R >= 1                                          */
+  int32_t num_q_heads;    /* Hq >= 1                                         */
+  int32_t num_kv_heads;   /* Hkv >= 1, Hq % Hkv == 0                         */
+  int32_t head_dim;       /* D: 64 or 128                                    */
+  int32_t page_size;      /* must be 16                                      */
+  int32_t num_pages;      /* pages in each cache pool                        */
+  float sm_scale;         /* softmax scale; <= 0 selects 1/sqrt(D)           */
+  const int32_t* q_indptr;     /* host [R+1], q_indptr[0] = 0, nondecreasing  */
+  const int32_t* n_verify;     /* host [R], 0 <= n_verify[r] <= n_r           */
+  const int32_t* ctx_len;      /* host [R], >= 0                              */
+  const int32_t* page_indptr;  /* host [R+1], page_indptr[0] = 0, nondecr.    */
+  const int32_t* page_indices; /* DEVICE [page_indptr[R]], each < num_pages   */
+} rg_attn_layout;
+
+/* Workspace bytes rg_draft_verify_attention needs for this layout (0 if no
+ * request is split across several KV chunks). */
+rg_status rg_draft_verify_attention_workspace(const rg_attn_layout* layout, size_t* bytes);
+
+/*
+ * Hybrid-mask attention of one fused draft-verify step.
+ *
+ *   q     DEVICE [q_indptr[R]][Hq][D] bf16
+ *   out   DEVICE [q_indptr[R]][Hq][D] bf16, softmax(scale*q.k + mask) . v,
+ *         fp32 accumulation, rounded to nearest even
+ *   lse   DEVICE [q_indptr[R]][Hq] fp32 natural-log log-sum-exp of the
+ *         scaled, masked scores, or NULL
+ *   ws    DEVICE workspace of at least the queried size (may be NULL when
+ *         that size is 0); its contents need no initialisation.
+ */
+rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t* q,
+                                    const uint16_t* k_cache, const uint16_t* v_cache,
+                                    uint16_t* out, float* lse, void* ws, size_t ws_bytes,
+                                    void* stream);
+
+/* Planning summary of an attention call (host only, no GPU work): used by
+ * tests and tools to inspect how the batch is split. */
+typedef struct rg_attn_plan_info {
+  int32_t num_launches;     /* launches of the main kernel                   */
+  int32_t chunk_keys;       /* keys per KV chunk                             */
+  int64_t work_items;       /* (request, kv head, column group, chunk) items */
+  int64_t split_requests;   /* requests whose keys span more than one chunk  */
+  int64_t partial_columns;  /* partial rows written to the workspace         */
+  int64_t workspace_bytes;
+} rg_attn_plan_info;
+rg_status rg_draft_verify_attention_plan(const rg_attn_layout* layout, rg_attn_plan_info* info);
+
+/*
+ * Greedy verification (Sec. 3.1; greedy decoding as in Sec. 6.1).
+ *
+ *   logits        DEVICE [total_rows] rows of `vocab` bf16 values, row k at
+ *                 logits + k * row_stride (row_stride >= vocab, elements)
+ *   row_indptr    DEVICE [R+1] int32: request r owns verify rows
+ *                 row_indptr[r] .. row_indptr[r+1]-1 (may be empty);
+ *                 row_indptr[0] = 0, row_indptr[R] = total_rows
+ *   draft_tokens  DEVICE [total_rows] int32: the token row k judges; a
+ *                 negative token marks a bonus row that never matches
+ * Outputs (DEVICE, int32 / fp32):
+ *   row_argmax     [total_rows]  lowest index of the row maximum
+ *   accept_len     [R]  first k < V_r with row_argmax != token, else V_r
+ *   next_token     [R]  row_argmax of row accept_len, or -1 if all matched
+ *   row_entropy    [total_rows] or NULL: entropy (nats) of softmax(row)
+ *   accept_entropy [R] or NULL: mean row entropy over rows
+ *                  0 .. min(accept_len, V_r - 1) (the e_t of Sec. 5.2);
+ *                  requests without rows get accept_len 0, next_token -1,
+ *                  accept_entropy 0.
+ */
+rg_status rg_verify_accept_workspace(int32_t num_requests, int32_t total_rows, int32_t vocab,
+                                     size_t* bytes);
+rg_status rg_verify_accept(const uint16_t* logits, int64_t row_stride, int32_t vocab,
+                           int32_t num_requests, int32_t total_rows, const int32_t* row_indptr,
+                           const int32_t* draft_tokens, int32_t* row_argmax, int32_t* accept_len,
+                           int32_t* next_token, float* row_entropy, float* accept_entropy,
+                           void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Draft confidence per row (Sec. 4.1), softmax at temperature 1.
+ *
+ *   logits  DEVICE [total_rows] rows of `vocab` bf16 values (vocab >= 2),
+ *           row k at logits + k * row_stride
+ * Outputs (DEVICE):
+ *   top1    [rows] int32  lowest index of the maximum
+ *   top2    [rows] int32  lowest index of the maximum over the other entries
+ *   p1      [rows] fp32   P_1st = softmax(row)[top1]   (confidence C_i)
+ *   p2      [rows] fp32   P_2nd = softmax(row)[top2]
+ *   margin  [rows] fp32 or NULL  P_1st - P_2nd          (margin M_i)
+ *   entropy [rows] fp32 or NULL  entropy (nats) of softmax(row)
+ */
+rg_status rg_draft_confidence_workspace(int32_t total_rows, int32_t vocab, size_t* bytes);
+rg_status rg_draft_confidence(const uint16_t* logits, int64_t row_stride, int32_t vocab,
+                              int32_t total_rows, int32_t* top1, int32_t* top2, float* p1,
+                              float* p2, float* margin, float* entropy, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/* Zero-fill `bytes` bytes of device memory at `ws` on `stream` with a
+ * kernel (no memset node), e.g. a fresh workspace before its first use. */
+rg_status rg_workspace_zero(void* ws, size_t bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RECGUIDE_H */

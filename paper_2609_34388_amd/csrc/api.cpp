@@ -1,0 +1,332 @@
+// C ABI of the draft-verify hot path: argument validation, planning of the
+// ragged attention batch, workspace carving and kernel launches.
+//
+// Planning reads only the host copies of the per-request sizes and turns
+// them into launch arguments (AttnPlan): no table is uploaded and nothing is
+// synchronised, so a call costs its kernel launches and nothing else on the
+// stream.
+#include "recguide.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <vector>
+
+#include "rg_internal.h"
+
+namespace {
+
+using namespace rg;
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+int env_int(const char* name, int fallback) {
+  const char* v = std::getenv(name);
+  if (v == nullptr || *v == 0) return fallback;
+  return std::atoi(v);
+}
+
+rg_status validate_layout(const rg_attn_layout* L) {
+  if (L == nullptr) return RG_ERR_NULL;
+  if (!L->q_indptr || !L->n_verify || !L->ctx_len || !L->page_indptr || !L->page_indices) return RG_ERR_NULL;
+  if (L->num_requests < 1 || L->num_q_heads < 1 || L->num_kv_heads < 1 || L->num_pages < 1) return RG_ERR_SHAPE;
+  if (L->num_q_heads % L->num_kv_heads != 0) return RG_ERR_SHAPE;
+  if (L->head_dim != 64 && L->head_dim != 128) return RG_ERR_UNSUPPORTED;
+  if (L->page_size != kPageSize) return RG_ERR_UNSUPPORTED;
+  if (L->q_indptr[0] != 0 || L->page_indptr[0] != 0) return RG_ERR_SHAPE;
+  for (int r = 0; r < L->num_requests; ++r) {
+    const int64_t n = (int64_t)L->q_indptr[r + 1] - L->q_indptr[r];
+    const int64_t pages = (int64_t)L->page_indptr[r + 1] - L->page_indptr[r];
+    if (n < 0 || pages < 0 || L->ctx_len[r] < 0) return RG_ERR_SHAPE;
+    if (L->n_verify[r] < 0 || L->n_verify[r] > n) return RG_ERR_SHAPE;
+    if (n > 0xffff) return RG_ERR_UNSUPPORTED;  // query rows per request
+    const int64_t T = (int64_t)L->ctx_len[r] + n;
+    if (T > (int64_t(1) << 30)) return RG_ERR_UNSUPPORTED;
+    if (n > 0 && pages * kPageSize < T) return RG_ERR_SHAPE;
+  }
+  return RG_OK;
+}
+
+struct FullPlan {
+  std::vector<AttnPlan> launches;
+  int chunk = 0;
+  int cols_per_group = 128;
+  int64_t items = 0, split_requests = 0, max_partial_cols = 0, total_partial_cols = 0;
+  size_t ws_bytes = 0;
+  size_t ml_offset = 0;
+};
+
+// Keys per work item: enough items to cover the 256 CUs a few times over,
+// but no smaller than the floor (small chunks multiply the partial outputs a
+// split request writes and re-reads: columns * D * 4 bytes per chunk against
+// chunk * D * 4 bytes of K/V).
+int choose_chunk(int64_t total_keys) {
+  const int forced = env_int("RG_ATTN_CHUNK", 0);
+  if (forced > 0) return (int)std::min<int64_t>(kMaxChunkKeys, round_up(forced, kKeyTile));
+  const int target = std::max(1, env_int("RG_ATTN_TARGET_ITEMS", 1024));
+  const int floor_keys = std::max(kKeyTile, env_int("RG_ATTN_MIN_CHUNK", 256));
+  int64_t chunk = round_up((total_keys + target - 1) / target, kKeyTile);
+  chunk = std::max<int64_t>(chunk, round_up(floor_keys, kKeyTile));
+  chunk = std::min<int64_t>(chunk, kMaxChunkKeys);
+  return (int)chunk;
+}
+
+rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
+  const int R = L->num_requests;
+  const int g = L->num_q_heads / L->num_kv_heads;
+  const int hkv = L->num_kv_heads;
+  int64_t max_cols = 0;
+  for (int r = 0; r < R; ++r) max_cols = std::max<int64_t>(max_cols, (int64_t)(L->q_indptr[r + 1] - L->q_indptr[r]) * g);
+  fp.cols_per_group = max_cols > 128 ? 256 : 128;
+  int64_t total_keys = 0;
+  for (int r = 0; r < R; ++r) {
+    const int64_t n = L->q_indptr[r + 1] - L->q_indptr[r];
+    if (n == 0) continue;
+    const int64_t ncg = (n * g + fp.cols_per_group - 1) / fp.cols_per_group;
+    total_keys += ((int64_t)L->ctx_len[r] + n) * hkv * ncg;
+  }
+  fp.chunk = choose_chunk(total_keys);
+  for (int r0 = 0; r0 < R; r0 += kMaxReqPerLaunch) {
+    const int cnt = std::min(kMaxReqPerLaunch, R - r0);
+    AttnPlan p;
+    std::memset(&p, 0, sizeof(p));
+    p.num_req = cnt;
+    p.chunk = fp.chunk;
+    p.cols_per_group = fp.cols_per_group;
+    int64_t items = 0, part = 0, comb = 0;
+    for (int k = 0; k < cnt; ++k) {
+      const int r = r0 + k;
+      const int64_t n = L->q_indptr[r + 1] - L->q_indptr[r];
+      AttnReq& q = p.req[k];
+      q.q_start = L->q_indptr[r];
+      q.ctx = L->ctx_len[r];
+      q.nv = (int32_t)(n | ((int64_t)L->n_verify[r] << 16));
+      q.page_start = L->page_indptr[r];
+      q.item_start = (int32_t)items;
+      q.part_start = (int32_t)part;
+      q.comb_start = (int32_t)comb;
+      if (n == 0) continue;
+      const int64_t M = n * g;
+      const int64_t T = (int64_t)L->ctx_len[r] + n;
+      const int64_t nch = (T + fp.chunk - 1) / fp.chunk;
+      const int64_t ncg = (M + fp.cols_per_group - 1) / fp.cols_per_group;
+      items += hkv * ncg * nch;
+      if (nch > 1) {
+        part += hkv * nch * M;
+        comb += hkv * ((M + 3) / 4);
+        fp.split_requests += 1;
+      }
+      if (items > INT32_MAX / 2 || part > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
+    }
+    p.req[cnt].item_start = (int32_t)items;
+    p.req[cnt].part_start = (int32_t)part;
+    p.req[cnt].comb_start = (int32_t)comb;
+    p.total_items = (int32_t)items;
+    p.total_comb = (int32_t)comb;
+    p.grid_items = (int32_t)round_up(items, 8);
+    p.grid_comb = (int32_t)round_up(comb, 8);
+    fp.items += items;
+    fp.max_partial_cols = std::max(fp.max_partial_cols, part);
+    fp.total_partial_cols += part;
+    fp.launches.push_back(p);
+  }
+  const size_t o_bytes = align256((size_t)fp.max_partial_cols * L->head_dim * sizeof(float));
+  fp.ml_offset = o_bytes;
+  fp.ws_bytes = fp.max_partial_cols ? o_bytes + align256((size_t)fp.max_partial_cols * 2 * sizeof(float)) : 0;
+  return RG_OK;
+}
+
+size_t verify_ws_bytes(int32_t R, int32_t rows, int32_t vocab) {
+  const size_t nchunk = logit_chunks(vocab);
+  return align256((size_t)rows * 4) + align256((size_t)R * 4) + align256((size_t)rows * nchunk * 16) +
+         align256((size_t)rows * 8);
+}
+
+size_t draft_ws_bytes(int32_t rows, int32_t vocab) {
+  const size_t nchunk = logit_chunks(vocab);
+  return align256((size_t)rows * 4) + align256((size_t)rows * nchunk * 16) + align256((size_t)rows * nchunk * 8);
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t rg_abi_version(void) { return RG_ABI_VERSION; }
+
+const char* rg_status_string(rg_status s) {
+  switch (s) {
+    case RG_OK: return "ok";
+    case RG_ERR_NULL: return "a required pointer is NULL";
+    case RG_ERR_SHAPE: return "inconsistent sizes or offsets";
+    case RG_ERR_UNSUPPORTED: return "unsupported configuration";
+    case RG_ERR_WORKSPACE: return "workspace missing or too small";
+    case RG_ERR_HIP: return "HIP launch or runtime error";
+    default: return "unknown status";
+  }
+}
+
+rg_status rg_draft_verify_attention_workspace(const rg_attn_layout* layout, size_t* bytes) {
+  if (bytes == nullptr) return RG_ERR_NULL;
+  rg_status st = validate_layout(layout);
+  if (st != RG_OK) return st;
+  FullPlan fp;
+  st = plan_attention(layout, fp);
+  if (st != RG_OK) return st;
+  *bytes = fp.ws_bytes;
+  return RG_OK;
+}
+
+rg_status rg_draft_verify_attention_plan(const rg_attn_layout* layout, rg_attn_plan_info* info) {
+  if (info == nullptr) return RG_ERR_NULL;
+  rg_status st = validate_layout(layout);
+  if (st != RG_OK) return st;
+  FullPlan fp;
+  st = plan_attention(layout, fp);
+  if (st != RG_OK) return st;
+  info->num_launches = (int32_t)fp.launches.size();
+  info->chunk_keys = fp.chunk;
+  info->work_items = fp.items;
+  info->split_requests = fp.split_requests;
+  info->partial_columns = fp.total_partial_cols;
+  info->workspace_bytes = (int64_t)fp.ws_bytes;
+  return RG_OK;
+}
+
+rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t* q,
+                                    const uint16_t* k_cache, const uint16_t* v_cache,
+                                    uint16_t* out, float* lse, void* ws, size_t ws_bytes,
+                                    void* stream) {
+  rg_status st = validate_layout(layout);
+  if (st != RG_OK) return st;
+  if (!q || !k_cache || !v_cache || !out) return RG_ERR_NULL;
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
+      (lse && !aligned(lse, 4)) || !aligned(layout->page_indices, 4))
+    return RG_ERR_UNSUPPORTED;
+  FullPlan fp;
+  st = plan_attention(layout, fp);
+  if (st != RG_OK) return st;
+  if (fp.ws_bytes > 0 && (ws == nullptr || ws_bytes < fp.ws_bytes || !aligned(ws, 16))) return RG_ERR_WORKSPACE;
+
+  AttnArgs a;
+  a.q = q;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.out = out;
+  a.lse = lse;
+  a.page_indices = layout->page_indices;
+  a.part_o = fp.ws_bytes ? static_cast<float*>(ws) : nullptr;
+  a.part_ml = fp.ws_bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + fp.ml_offset) : nullptr;
+  a.hq = layout->num_q_heads;
+  a.hkv = layout->num_kv_heads;
+  a.g = layout->num_q_heads / layout->num_kv_heads;
+  a.sm_scale = layout->sm_scale > 0.f ? layout->sm_scale : 1.0f / std::sqrt((float)layout->head_dim);
+  a.scale_log2 = a.sm_scale * 1.4426950408889634f;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (const AttnPlan& p : fp.launches) {
+    if (p.total_items == 0) continue;
+    if (launch_attention(a, p, layout->head_dim, s) != hipSuccess) return RG_ERR_HIP;
+  }
+  return RG_OK;
+}
+
+rg_status rg_verify_accept_workspace(int32_t num_requests, int32_t total_rows, int32_t vocab, size_t* bytes) {
+  if (bytes == nullptr) return RG_ERR_NULL;
+  if (num_requests < 1 || total_rows < 0 || vocab < 1) return RG_ERR_SHAPE;
+  *bytes = verify_ws_bytes(num_requests, total_rows, vocab);
+  return RG_OK;
+}
+
+rg_status rg_verify_accept(const uint16_t* logits, int64_t row_stride, int32_t vocab,
+                           int32_t num_requests, int32_t total_rows, const int32_t* row_indptr,
+                           const int32_t* draft_tokens, int32_t* row_argmax, int32_t* accept_len,
+                           int32_t* next_token, float* row_entropy, float* accept_entropy,
+                           void* ws, size_t ws_bytes, void* stream) {
+  if (num_requests < 1 || total_rows < 0 || vocab < 1) return RG_ERR_SHAPE;
+  if (!row_indptr || !accept_len || !next_token) return RG_ERR_NULL;
+  if (total_rows > 0 && (!logits || !draft_tokens || !row_argmax)) return RG_ERR_NULL;
+  if (row_stride < vocab) return RG_ERR_SHAPE;
+  if ((int64_t)total_rows * logit_chunks(vocab) > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
+  const size_t need = verify_ws_bytes(num_requests, total_rows, vocab);
+  if (ws == nullptr || ws_bytes < need || !aligned(ws, 16)) return RG_ERR_WORKSPACE;
+
+  VerifyArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.logits = logits;
+  a.row_stride = row_stride;
+  a.vocab = vocab;
+  a.num_req = num_requests;
+  a.rows = total_rows;
+  a.nchunk = logit_chunks(vocab);
+  a.row_indptr = row_indptr;
+  a.tokens = draft_tokens;
+  a.row_argmax = row_argmax;
+  a.accept_len = accept_len;
+  a.next_token = next_token;
+  a.row_entropy = row_entropy;
+  a.accept_entropy = accept_entropy;
+  char* w = static_cast<char*>(ws);
+  a.row_cnt = reinterpret_cast<int32_t*>(w);
+  w += align256((size_t)total_rows * 4);
+  a.req_cnt = reinterpret_cast<int32_t*>(w);
+  w += align256((size_t)num_requests * 4);
+  a.chunk_st = reinterpret_cast<float4*>(w);
+  w += align256((size_t)total_rows * a.nchunk * 16);
+  a.row_st = reinterpret_cast<float2*>(w);
+  a.vec = (aligned(logits, 16) && row_stride % 8 == 0) ? 1 : 0;
+  a.grid_rows = (int32_t)round_up((int64_t)total_rows * a.nchunk, 8);
+  return launch_verify(a, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
+
+rg_status rg_draft_confidence_workspace(int32_t total_rows, int32_t vocab, size_t* bytes) {
+  if (bytes == nullptr) return RG_ERR_NULL;
+  if (total_rows < 0 || vocab < 2) return RG_ERR_SHAPE;
+  *bytes = draft_ws_bytes(total_rows, vocab);
+  return RG_OK;
+}
+
+rg_status rg_draft_confidence(const uint16_t* logits, int64_t row_stride, int32_t vocab,
+                              int32_t total_rows, int32_t* top1, int32_t* top2, float* p1,
+                              float* p2, float* margin, float* entropy, void* ws,
+                              size_t ws_bytes, void* stream) {
+  if (total_rows < 0 || vocab < 2) return RG_ERR_SHAPE;
+  if (total_rows > 0 && (!logits || !top1 || !top2 || !p1 || !p2)) return RG_ERR_NULL;
+  if (row_stride < vocab) return RG_ERR_SHAPE;
+  if ((int64_t)total_rows * logit_chunks(vocab) > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
+  const size_t need = draft_ws_bytes(total_rows, vocab);
+  if (total_rows > 0 && (ws == nullptr || ws_bytes < need || !aligned(ws, 16))) return RG_ERR_WORKSPACE;
+  if (total_rows == 0) return RG_OK;
+
+  DraftArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.logits = logits;
+  a.row_stride = row_stride;
+  a.vocab = vocab;
+  a.rows = total_rows;
+  a.nchunk = logit_chunks(vocab);
+  a.top1 = top1;
+  a.top2 = top2;
+  a.p1 = p1;
+  a.p2 = p2;
+  a.margin = margin;
+  a.entropy = entropy;
+  char* w = static_cast<char*>(ws);
+  a.row_cnt = reinterpret_cast<int32_t*>(w);
+  w += align256((size_t)total_rows * 4);
+  a.chunk_a = reinterpret_cast<float4*>(w);
+  w += align256((size_t)total_rows * a.nchunk * 16);
+  a.chunk_b = reinterpret_cast<float2*>(w);
+  a.vec = (aligned(logits, 16) && row_stride % 8 == 0) ? 1 : 0;
+  a.grid_rows = (int32_t)round_up((int64_t)total_rows * a.nchunk, 8);
+  return launch_draft(a, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
+
+rg_status rg_workspace_zero(void* ws, size_t bytes, void* stream) {
+  if (bytes == 0) return RG_OK;
+  if (ws == nullptr) return RG_ERR_NULL;
+  return launch_zero(ws, bytes, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
+
+}  // extern "C"

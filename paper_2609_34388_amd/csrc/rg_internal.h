@@ -1,0 +1,110 @@
+// Internal launch-side structures shared by the host API and the kernels.
+// Not part of the public ABI (include/recguide.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace rg {
+
+constexpr int kPageSize = 16;
+constexpr int kMaxReqPerLaunch = 128;  // equals RG_ATTN_MAX_REQS_PER_LAUNCH
+constexpr int kKeyTile = 64;           // keys staged in LDS per step
+constexpr int kMaxChunkKeys = 8192;    // keys per work item at most
+constexpr int kAttnThreads = 256;      // 4 waves of 64
+
+// Per-request data of one attention launch.  Everything a work group needs
+// about its request travels in the kernel arguments, so no table has to be
+// copied to the device before the kernels run.
+struct AttnReq {
+  int32_t q_start;     // first query row (token) of the request
+  int32_t ctx;         // cached context tokens L
+  int32_t nv;          // n (low 16 bits) | n_verify << 16
+  int32_t page_start;  // offset of the request's pages in page_indices
+  int32_t item_start;  // first main-kernel work item
+  int32_t part_start;  // first partial column in the workspace (split requests)
+  int32_t comb_start;  // first combine work item (split requests)
+};
+
+struct AttnPlan {
+  int32_t num_req;         // requests in this launch
+  int32_t chunk;           // keys per work item, multiple of kKeyTile
+  int32_t total_items;     // main-kernel work items
+  int32_t total_comb;      // combine work items
+  int32_t grid_items;      // total_items rounded up to a multiple of 8
+  int32_t grid_comb;       // total_comb rounded up to a multiple of 8
+  int32_t cols_per_group;  // query columns one work group covers (128 or 256)
+  int32_t pad;
+  AttnReq req[kMaxReqPerLaunch + 1];  // entry num_req holds the end sentinels
+};
+static_assert(sizeof(AttnPlan) <= 3700, "attention plan must fit the kernel argument block");
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k_cache;
+  const uint16_t* v_cache;
+  uint16_t* out;
+  float* lse;
+  const int32_t* page_indices;
+  float* part_o;   // [partial columns][D] fp32, un-normalised
+  float* part_ml;  // [partial columns][2] fp32 (running max of raw scores, sum)
+  int32_t hq, hkv, g;
+  float sm_scale;    // natural-log domain scale
+  float scale_log2;  // sm_scale * log2(e)
+};
+
+// Attention launchers (attention.hip).  `plan` is one launch's plan.
+hipError_t launch_attention(const AttnArgs& args, const AttnPlan& plan, int head_dim,
+                            hipStream_t stream);
+
+// Logit-row reductions (logits.hip).
+constexpr int kLogitThreads = 256;
+constexpr int kLogitChunk = 8192;  // vocab entries per work group
+
+struct VerifyArgs {
+  const uint16_t* logits;
+  int64_t row_stride;
+  int32_t vocab, num_req, rows, nchunk;
+  const int32_t* row_indptr;
+  const int32_t* tokens;
+  int32_t* row_argmax;
+  int32_t* accept_len;
+  int32_t* next_token;
+  float* row_entropy;
+  float* accept_entropy;
+  // workspace carve-up
+  int32_t* row_cnt;    // [rows]
+  int32_t* req_cnt;    // [num_req]
+  float4* chunk_st;    // [rows * nchunk] (max, bits(argmax), Z', S)
+  float2* row_st;      // [rows] (bits(argmax), entropy)
+  int32_t vec;         // 16-byte loads allowed
+  int32_t grid_rows;   // row work groups (rows * nchunk rounded up to 8)
+};
+
+struct DraftArgs {
+  const uint16_t* logits;
+  int64_t row_stride;
+  int32_t vocab, rows, nchunk;
+  int32_t* top1;
+  int32_t* top2;
+  float* p1;
+  float* p2;
+  float* margin;
+  float* entropy;
+  int32_t* row_cnt;      // [rows]
+  float4* chunk_a;       // [rows * nchunk] (max, bits(i1), v2, bits(i2))
+  float2* chunk_b;       // [rows * nchunk] (Z', S)
+  int32_t vec;
+  int32_t grid_rows;
+};
+
+inline int32_t logit_chunks(int32_t vocab) { return (vocab + kLogitChunk - 1) / kLogitChunk; }
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream);
+hipError_t launch_draft(const DraftArgs& a, hipStream_t stream);
+hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t stream);
+
+}  // namespace rg

@@ -1,0 +1,192 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/recguide.h declares, rejects bad arguments with the documented
+status before touching the device, and plans ragged batches consistently."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_34388_amd import binding
+from paper_2609_34388_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "recguide.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(binding.LIB_PATH), reason="library not built")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(rg_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_exports_every_declared_function():
+    lib = binding.library()
+    names = _declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(binding.EXPORTS)
+
+
+def test_abi_version_and_status_strings():
+    m = re.search(r"#define RG_ABI_VERSION (\d+)", open(HEADER).read())
+    assert binding.abi_version() == int(m.group(1))
+    lib = binding.library()
+    for s in range(6):
+        assert lib.rg_status_string(s)
+    assert lib.rg_status_string(99) == b"unknown status"
+
+
+FAKE_DEV = ctypes.c_void_p(0x1000)  # never dereferenced on the validation paths
+
+
+class _L:
+    def __init__(self, R=2, hq=8, hkv=2, D=128, page=16, num_pages=64, ctx=(40, 17), nv=(3, 0), n=(7, 5),
+                 pages=None):
+        self.q_indptr = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+        self.n_verify = np.asarray(nv, dtype=np.int32)
+        self.ctx_len = np.asarray(ctx, dtype=np.int32)
+        if pages is None:
+            pages = [math.ceil((c + k) / 16) for c, k in zip(ctx, n)]
+        self.page_indptr = np.concatenate([[0], np.cumsum(pages)]).astype(np.int32)
+        self.c = binding.AttnLayout(R, hq, hkv, D, page, num_pages, 0.0, self.q_indptr.ctypes.data,
+                                    self.n_verify.ctypes.data, self.ctx_len.ctypes.data,
+                                    self.page_indptr.ctypes.data, FAKE_DEV.value)
+
+
+def _attn(l, q=FAKE_DEV, k=FAKE_DEV, v=FAKE_DEV, out=FAKE_DEV):
+    return binding.library().rg_draft_verify_attention(ctypes.byref(l.c), q, k, v, out, None, None, 0, None)
+
+
+def test_attention_validation_errors():
+    lib = binding.library()
+    assert lib.rg_draft_verify_attention(None, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV, None, None, 0, None) == 1
+    assert _attn(_L(), q=None) == 1
+    assert _attn(_L(), out=None) == 1
+    l = _L(); l.c.num_requests = 0
+    assert _attn(l) == 2
+    l = _L(); l.c.num_q_heads = 6; l.c.num_kv_heads = 4
+    assert _attn(l) == 2
+    l = _L(); l.c.head_dim = 96
+    assert _attn(l) == 3
+    l = _L(); l.c.page_size = 32
+    assert _attn(l) == 3
+    assert _attn(_L(nv=(8, 0))) == 2                       # more verify rows than rows
+    assert _attn(_L(ctx=(-1, 3))) == 2
+    assert _attn(_L(pages=[2, 2])) == 2                    # too few pages for 47 keys
+    l = _L(); l.page_indptr[0] = 1
+    assert _attn(l) == 2
+    l = _L(); l.c.page_indices = None
+    assert _attn(l) == 1
+    # misaligned pointers are rejected, not read
+    assert _attn(_L(), q=ctypes.c_void_p(0x1002)) == 3
+
+
+def test_logit_validation_errors():
+    lib = binding.library()
+    ws = ctypes.c_void_p(0x2000)
+    n = ctypes.c_size_t()
+    assert lib.rg_verify_accept_workspace(0, 4, 100, ctypes.byref(n)) == 2
+    assert lib.rg_verify_accept_workspace(1, 4, 100, None) == 1
+    assert lib.rg_verify_accept_workspace(2, 4, 20000, ctypes.byref(n)) == 0 and n.value > 0
+    need = n.value
+    args = [FAKE_DEV, 20000, 20000, 2, 4, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV, None, None]
+    assert lib.rg_verify_accept(*args, ws, need - 1, None) == 4
+    assert lib.rg_verify_accept(*args[:1], 100, 20000, *args[3:], ws, need, None) == 2  # stride < vocab
+    bad = list(args); bad[5] = None
+    assert lib.rg_verify_accept(*bad, ws, need, None) == 1
+    assert lib.rg_draft_confidence_workspace(4, 1, ctypes.byref(n)) == 2
+    assert lib.rg_draft_confidence_workspace(4, 2, ctypes.byref(n)) == 0
+    need = n.value
+    dargs = [FAKE_DEV, 2, 2, 4, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV, None, None]
+    assert lib.rg_draft_confidence(*dargs, ws, need - 1, None) == 4
+    dargs[4] = None
+    assert lib.rg_draft_confidence(*dargs, ws, need, None) == 1
+    assert lib.rg_workspace_zero(None, 16, None) == 1
+    assert lib.rg_workspace_zero(None, 0, None) == 0
+
+
+def _plan(l):
+    info = binding.AttnPlanInfo()
+    assert binding.library().rg_draft_verify_attention_plan(ctypes.byref(l.c), ctypes.byref(info)) == 0
+    return info
+
+
+@pytest.mark.parametrize("name", ["tiny", "low", "mid", "high", "long"])
+def test_plan_accounting(name):
+    lay = W.make_layout(name, seed=1)
+    s = lay.spec
+    l = _L(R=lay.num_requests, hq=s.num_q_heads, hkv=s.num_kv_heads, D=s.head_dim,
+           num_pages=lay.num_pages, ctx=lay.ctx_len, nv=lay.n_verify, n=lay.q_len,
+           pages=np.diff(lay.page_indptr))
+    info = _plan(l)
+    g = s.num_q_heads // s.num_kv_heads
+    ch = info.chunk_keys
+    assert ch % 64 == 0 and 64 <= ch <= 8192
+    cpg = 256 if (lay.q_len * g).max() > 128 else 128
+    items = split = part = 0
+    for r in range(lay.num_requests):
+        T, M = int(lay.kv_len[r]), int(lay.q_len[r]) * g
+        nch = -(-T // ch)
+        items += s.num_kv_heads * (-(-M // cpg)) * nch
+        if nch > 1:
+            split += 1
+            part += s.num_kv_heads * nch * M
+    assert info.work_items == items
+    assert info.split_requests == split
+    assert info.partial_columns == part
+    assert info.num_launches == -(-lay.num_requests // 128)
+    if part:
+        assert info.workspace_bytes >= part // info.num_launches * s.head_dim * 4
+    else:
+        assert info.workspace_bytes == 0
+
+
+def test_plan_chunk_override_and_workspace_monotone(monkeypatch):
+    lay = W.make_layout("mid", seed=2)
+    s = lay.spec
+    mk = lambda: _L(R=lay.num_requests, hq=s.num_q_heads, hkv=s.num_kv_heads, D=s.head_dim,
+                    num_pages=lay.num_pages, ctx=lay.ctx_len, nv=lay.n_verify, n=lay.q_len,
+                    pages=np.diff(lay.page_indptr))
+    sizes = []
+    for ch in (8192, 2048, 512, 128):
+        monkeypatch.setenv("RG_ATTN_CHUNK", str(ch))
+        info = _plan(mk())
+        assert info.chunk_keys == ch
+        sizes.append(info.workspace_bytes)
+    assert sizes == sorted(sizes)
+
+
+def test_generators_are_deterministic():
+    a = W.make_layout("high", seed=5)
+    b = W.make_layout("high", seed=5)
+    for f in ("ctx_len", "n_verify", "n_draft", "page_indices", "q_indptr"):
+        np.testing.assert_array_equal(getattr(a, f), getattr(b, f))
+    c = W.make_layout("high", seed=6)
+    assert not np.array_equal(a.ctx_len, c.ctx_len)
+    small = W.make_layout("tiny", seed=3)
+    x = W.make_attention_inputs(small)
+    y = W.make_attention_inputs(small)
+    for k in x:
+        np.testing.assert_array_equal(W.bf16_bits(x[k]), W.bf16_bits(y[k]))
+    lx = W.make_logit_inputs(small)
+    ly = W.make_logit_inputs(small)
+    for k in lx:
+        assert np.array_equal(lx[k].view(-1).float().numpy(), ly[k].view(-1).float().numpy())
+
+
+def test_generated_layout_respects_spec_ranges():
+    lay = W.make_layout("long", seed=0)
+    assert lay.num_requests == 64
+    assert lay.ctx_len.min() >= 16384 and lay.ctx_len.max() <= 32768
+    assert set(np.unique(lay.n_verify)) <= {4, 8, 16, 32}
+    # every page referenced once, random order
+    assert len(np.unique(lay.page_indices)) == len(lay.page_indices)
+    assert lay.page_indices.max() < lay.num_pages
+    pages = np.diff(lay.page_indptr)
+    assert (pages * 16 >= lay.kv_len).all() and ((pages - 1) * 16 < lay.kv_len).all()

@@ -1,0 +1,200 @@
+"""GPU parity of rg_draft_verify_attention against the fp64 oracle.
+
+Tolerance (per output row and query head): max_d |gpu - oracle| <=
+1e-2 * ||oracle row||_2 (floor 1e-6), lse within 1e-3 absolute.  Inputs are
+the same bf16 bits on both sides; unused cache slots and pages are poisoned
+with NaN so that any out-of-range read shows up.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_34388_amd import binding
+from paper_2609_34388_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda")
+ATOL_ROW = 1e-2
+LSE_ATOL = 1e-3
+
+
+def run(lay, inp, **kw):
+    page_idx = torch.as_tensor(lay.page_indices, device=DEV)
+    out, lse = binding.draft_verify_attention(inp["q"], inp["k_cache"], inp["v_cache"], lay.q_indptr,
+                                              lay.n_verify, lay.ctx_len, lay.page_indptr, page_idx, **kw)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def reference(lay, inp, requests=None):
+    return oracle.oracle_attention(W.bf16_bits(inp["q"]), W.bf16_bits(inp["k_cache"]),
+                                   W.bf16_bits(inp["v_cache"]), lay.q_indptr, lay.n_verify,
+                                   lay.ctx_len, lay.page_indptr, lay.page_indices, requests=requests)
+
+
+def check(out, lse, ref, rows=None):
+    got = out.double().cpu().numpy()
+    want = ref["out"]
+    if rows is not None:
+        got, want = got[rows], want[rows]
+        gl, wl = lse.double().cpu().numpy()[rows], ref["lse"][rows]
+    else:
+        gl, wl = lse.double().cpu().numpy(), ref["lse"]
+    assert np.isfinite(got).all()
+    norm = np.maximum(np.linalg.norm(want, axis=-1), 1e-6)
+    err = np.abs(got - want).max(axis=-1) / norm
+    assert err.max() <= ATOL_ROW, f"max row error {err.max():.3e} at {np.unravel_index(err.argmax(), err.shape)}"
+    assert np.abs(gl - wl).max() <= LSE_ATOL
+    return err.max()
+
+
+def _custom(R, ctx, nv, nd, hq=8, hkv=2, D=128, seed=0):
+    spec = W.WorkloadSpec("custom", 9, R, hq, hkv, D, 1024, ("fixed", 0), ("fixed", 0), ("fixed", 0),
+                          ("fixed", 1.0), 1.0 / np.sqrt(D))
+    lay = W.make_layout(spec, seed=seed)
+    lay.ctx_len = np.asarray(ctx, dtype=np.int32)
+    lay.n_verify = np.asarray(nv, dtype=np.int32)
+    lay.n_draft = np.asarray(nd, dtype=np.int32)
+    q_len = lay.n_verify + lay.n_draft
+    T = lay.ctx_len + q_len
+    pages = (T + 15) // 16
+    lay.q_indptr = np.concatenate([[0], np.cumsum(q_len)]).astype(np.int32)
+    lay.page_indptr = np.concatenate([[0], np.cumsum(pages)]).astype(np.int32)
+    lay.num_pages = int(pages.sum()) + 5
+    lay.page_indices = np.random.default_rng(seed).permutation(lay.num_pages)[:pages.sum()].astype(np.int32)
+    lay.row_indptr = np.concatenate([[0], np.cumsum(lay.n_verify)]).astype(np.int32)
+    lay.draft_row_indptr = np.concatenate([[0], np.cumsum(lay.n_draft)]).astype(np.int32)
+    return lay
+
+
+def test_tiny_config_full():
+    lay = W.make_layout("tiny", seed=0)
+    inp = W.make_attention_inputs(lay, DEV, poison=float("nan"))
+    out, lse = run(lay, inp)
+    check(out, lse, reference(lay, inp))
+
+
+@pytest.mark.parametrize("kind,seed", [("mid", 1), ("high", 2), ("long", 3)])
+def test_scaled_down_configs_full(kind, seed):
+    kw = dict(mid=dict(num_requests=5, ctx=("uniform", 100, 700)),
+              high=dict(num_requests=12, ctx=("uniform", 30, 300)),
+              long=dict(num_requests=3, ctx=("uniform", 1500, 3000)))[kind]
+    lay = W.make_layout(kind, seed=seed, **kw)
+    inp = W.make_attention_inputs(lay, DEV, poison=float("nan"))
+    out, lse = run(lay, inp)
+    check(out, lse, reference(lay, inp))
+
+
+@pytest.mark.parametrize("case", [
+    dict(ctx=[0], nv=[3], nd=[5]),                       # empty context
+    dict(ctx=[37], nv=[0], nd=[6]),                      # draft rows only
+    dict(ctx=[50], nv=[7], nd=[0]),                      # verify rows only
+    dict(ctx=[0], nv=[0], nd=[1]),                       # one key
+    dict(ctx=[5], nv=[1], nd=[0]),                       # T < page
+    dict(ctx=[300], nv=[16], nd=[24]),                   # 160 columns: two tiles per wave
+    dict(ctx=[129], nv=[32], nd=[38]),                   # 280 columns: two column groups
+    dict(ctx=[64, 0, 200], nv=[4, 0, 9], nd=[4, 0, 7]),  # an empty request in the middle
+    dict(ctx=[1000], nv=[2], nd=[2], hq=4, hkv=4),       # g = 1
+    dict(ctx=[700, 33], nv=[8, 3], nd=[8, 2], D=64, hq=4, hkv=1),
+])
+def test_edge_cases(case):
+    kw = {k: case[k] for k in ("hq", "hkv", "D") if k in case}
+    R = len(case["ctx"])
+    lay = _custom(R, case["ctx"], case["nv"], case["nd"], **kw)
+    inp = W.make_attention_inputs(lay, DEV, poison=float("nan"))
+    out, lse = run(lay, inp)
+    check(out, lse, reference(lay, inp))
+
+
+@pytest.mark.parametrize("chunk", ["64", "128", "320", "1024"])
+def test_split_kv_chunks(monkeypatch, chunk):
+    monkeypatch.setenv("RG_ATTN_CHUNK", chunk)
+    lay = W.make_layout("mid", seed=4, num_requests=4, ctx=("uniform", 200, 1500))
+    inp = W.make_attention_inputs(lay, DEV, poison=float("nan"))
+    info = binding.attention_plan(binding.make_layout(inp["q"], inp["k_cache"], lay.q_indptr, lay.n_verify,
+                                                      lay.ctx_len, lay.page_indptr,
+                                                      torch.as_tensor(lay.page_indices, device=DEV)))
+    assert info["chunk_keys"] == int(chunk)
+    out, lse = run(lay, inp)
+    check(out, lse, reference(lay, inp))
+
+
+def test_many_requests_several_launches():
+    lay = W.make_layout("high", seed=5, num_requests=300, ctx=("uniform", 16, 100))
+    inp = W.make_attention_inputs(lay, DEV, poison=float("nan"))
+    out, lse = run(lay, inp)
+    check(out, lse, reference(lay, inp))
+
+
+@pytest.mark.parametrize("kind", ["tiny", "mid"])
+def test_mask_probe(kind):
+    kw = {} if kind == "tiny" else dict(num_requests=4, ctx=("uniform", 500, 900))
+    lay = W.make_layout(kind, seed=6, **kw)
+    inp = W.make_mask_probe(lay, DEV)
+    out, lse = run(lay, inp)
+    check(out, lse, reference(lay, inp))
+
+
+def test_sharp_scores():
+    lay = W.make_layout("mid", seed=7, num_requests=3, ctx=("uniform", 100, 400))
+    inp = W.make_attention_inputs(lay, DEV, poison=float("nan"), qk_std=1.0)
+    out, lse = run(lay, inp)
+    check(out, lse, reference(lay, inp))
+
+
+def test_poison_large_values_do_not_leak():
+    lay = W.make_layout("mid", seed=8, num_requests=3, ctx=("uniform", 100, 400))
+    inp = W.make_attention_inputs(lay, DEV, poison=1e4)
+    out, lse = run(lay, inp)
+    check(out, lse, reference(lay, inp))
+
+
+def test_deterministic_and_shuffle_invariant():
+    lay = W.make_layout("mid", seed=9, num_requests=3, ctx=("uniform", 300, 900))
+    inp = W.make_attention_inputs(lay, DEV)
+    a, la = run(lay, inp)
+    b, lb = run(lay, inp)
+    assert torch.equal(a, b) and torch.equal(la, lb)
+    # the same logical cache under another page assignment gives identical bits
+    perm = np.random.default_rng(0).permutation(lay.num_pages)
+    k2 = torch.empty_like(inp["k_cache"])
+    v2 = torch.empty_like(inp["v_cache"])
+    pt = torch.as_tensor(perm, device=DEV)
+    k2[pt] = inp["k_cache"]
+    v2[pt] = inp["v_cache"]
+    lay2 = W.make_layout("mid", seed=9, num_requests=3, ctx=("uniform", 300, 900))
+    lay2.page_indices = perm[lay.page_indices].astype(np.int32)
+    c, lc = run(lay2, dict(q=inp["q"], k_cache=k2, v_cache=v2))
+    assert torch.equal(a, c) and torch.equal(la, lc)
+
+
+def _sub_problem(lay, inp, r):
+    """One request of a large batch as a stand-alone problem (test plumbing:
+    its pages gathered on the GPU and renumbered 0..p-1)."""
+    p0, p1 = int(lay.page_indptr[r]), int(lay.page_indptr[r + 1])
+    pages = torch.as_tensor(lay.page_indices[p0:p1].astype(np.int64), device=DEV)
+    q0, q1 = int(lay.q_indptr[r]), int(lay.q_indptr[r + 1])
+    sub = dict(q=inp["q"][q0:q1], k_cache=inp["k_cache"][pages], v_cache=inp["v_cache"][pages])
+    return sub, np.array([0, q1 - q0]), np.array([0, p1 - p0]), np.arange(p1 - p0, dtype=np.int32)
+
+
+@pytest.mark.parametrize("name,samples", [("low", 1), ("mid", 3), ("high", 6), ("long", 2)])
+def test_full_size_configs_sampled(name, samples):
+    """Full benchmark shapes, launched exactly as the benchmark launches them;
+    the oracle recomputes a sample of requests (all heads, all rows)."""
+    lay = W.make_layout(name, seed=0)
+    inp = W.make_attention_inputs(lay, DEV, poison=float("nan"))
+    out, lse = run(lay, inp)
+    assert torch.isfinite(out.float()).all()
+    rng = np.random.default_rng(11)
+    reqs = sorted(set(rng.choice(lay.num_requests, size=min(samples, lay.num_requests), replace=False)))
+    if lay.num_requests > 1:
+        reqs = sorted(set(reqs) | {int(np.argmax(lay.kv_len)), int(np.argmax(lay.q_len))})
+    for r in reqs:
+        sub, qi, pi, pidx = _sub_problem(lay, inp, r)
+        ref = oracle.oracle_attention(W.bf16_bits(sub["q"]), W.bf16_bits(sub["k_cache"]),
+                                      W.bf16_bits(sub["v_cache"]), qi, lay.n_verify[r:r + 1],
+                                      lay.ctx_len[r:r + 1], pi, pidx)
+        q0, q1 = int(lay.q_indptr[r]), int(lay.q_indptr[r + 1])
+        check(out[q0:q1], lse[q0:q1], ref)

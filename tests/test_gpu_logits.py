@@ -1,0 +1,153 @@
+"""GPU parity of rg_verify_accept and rg_draft_confidence against the fp64
+oracle.
+
+Integer outputs (argmax, top-1/top-2 indices, accept lengths, next tokens)
+must be bit-exact, ties broken to the lowest index.  p1, p2, entropies and
+e_t within 1e-4 relative; the margin within 1e-4 * p1 absolute (it is a
+difference); p2 gets an absolute floor of 1e-30 (fp32 underflow).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_34388_amd import binding
+from paper_2609_34388_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda")
+RTOL = 1e-4
+
+
+def rel_ok(got, want, rtol=RTOL, floor=0.0):
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    bad = np.abs(got - want) > rtol * np.abs(want) + floor
+    assert not bad.any(), f"{bad.sum()} mismatches, worst got {got[bad][:3]} want {want[bad][:3]}"
+
+
+def check_verify(logits, row_indptr, tokens, res):
+    ref = oracle.oracle_accept(W.bf16_bits(logits), row_indptr, tokens.cpu().numpy())
+    np.testing.assert_array_equal(res["row_argmax"].cpu().numpy(), ref["row_argmax"])
+    np.testing.assert_array_equal(res["accept_len"].cpu().numpy(), ref["accept_len"])
+    np.testing.assert_array_equal(res["next_token"].cpu().numpy(), ref["next_token"])
+    rel_ok(res["row_entropy"].cpu().numpy(), ref["row_entropy"])
+    rel_ok(res["accept_entropy"].cpu().numpy(), ref["accept_entropy"], floor=1e-30)
+
+
+def check_draft(logits, res):
+    ref = oracle.oracle_confidence(W.bf16_bits(logits))
+    np.testing.assert_array_equal(res["top1"].cpu().numpy(), ref["top1"])
+    np.testing.assert_array_equal(res["top2"].cpu().numpy(), ref["top2"])
+    rel_ok(res["p1"].cpu().numpy(), ref["p1"])
+    rel_ok(res["p2"].cpu().numpy(), ref["p2"], floor=1e-30)
+    m = res["margin"].double().cpu().numpy()
+    assert (np.abs(m - ref["margin"]) <= RTOL * ref["p1"]).all()
+    rel_ok(res["entropy"].cpu().numpy(), ref["entropy"])
+
+
+def run_verify(lay, inp, **kw):
+    rp = torch.as_tensor(lay.row_indptr, device=DEV)
+    res = binding.verify_accept(inp["verify_logits"], rp, inp["draft_tokens"], **kw)
+    torch.cuda.synchronize()
+    return res
+
+
+def run_draft(logits, **kw):
+    res = binding.draft_confidence(logits, **kw)
+    torch.cuda.synchronize()
+    return res
+
+
+@pytest.mark.parametrize("name", ["tiny", "low", "low_sigma2", "mid", "high", "long"])
+def test_configs_full(name):
+    lay = W.make_layout(name, seed=0)
+    inp = W.make_logit_inputs(lay, DEV)
+    res = run_verify(lay, inp)
+    check_verify(inp["verify_logits"], lay.row_indptr, inp["draft_tokens"], res)
+    check_draft(inp["draft_logits"], run_draft(inp["draft_logits"]))
+
+
+@pytest.mark.parametrize("variant", ["sigma0", "ties", "spike", "bonus"])
+def test_variants(variant):
+    kw = dict(num_requests=6)
+    lay = W.make_layout("mid", seed=3, bonus_rows=(variant == "bonus"), **kw)
+    inp = W.make_logit_inputs(lay, DEV, sigma=0.0 if variant in ("sigma0", "bonus") else None,
+                              ties=(variant == "ties"), spike=12.0 if variant == "spike" else None)
+    res = run_verify(lay, inp)
+    check_verify(inp["verify_logits"], lay.row_indptr, inp["draft_tokens"], res)
+    if variant == "sigma0":
+        assert (res["accept_len"].cpu().numpy() == lay.n_verify).all()
+    check_draft(inp["draft_logits"], run_draft(inp["draft_logits"]))
+
+
+def test_peaked_rows_entropy_accuracy():
+    g = torch.Generator(device=DEV).manual_seed(1)
+    x = torch.randn(64, 50000, generator=g, device=DEV) * 2.0
+    x[torch.arange(64), torch.arange(64) * 700] += torch.linspace(5, 60, 64, device=DEV)
+    logits = x.to(torch.bfloat16)
+    check_draft(logits, run_draft(logits))
+
+
+@pytest.mark.parametrize("vocab", [2, 7, 1000, 8192, 8193, 128250])
+def test_vocab_sizes_and_tails(vocab):
+    g = torch.Generator(device=DEV).manual_seed(vocab)
+    logits = (torch.randn(9, vocab, generator=g, device=DEV) * 2).to(torch.bfloat16)
+    logits[3] = 0.0  # all tied
+    check_draft(logits, run_draft(logits))
+    rp = torch.tensor([0, 4, 4, 9], dtype=torch.int32, device=DEV)
+    tok = torch.argmax(logits.float(), dim=1).to(torch.int32)
+    tok[6] = (tok[6] + 1) % vocab
+    res = binding.verify_accept(logits, rp, tok)
+    torch.cuda.synchronize()
+    check_verify(logits, rp.cpu().numpy(), tok, res)
+
+
+def test_row_stride_and_unaligned_rows():
+    g = torch.Generator(device=DEV).manual_seed(5)
+    base = (torch.randn(12, 20011, generator=g, device=DEV) * 2).to(torch.bfloat16)
+    strided = base[:, :20000]            # row stride 20011 > vocab, rows not 16-byte aligned
+    assert strided.stride(0) == 20011
+    check_draft(strided, run_draft(strided))
+    shifted = base.view(-1)[1:1 + 12 * 20000].view(12, 20000)  # misaligned base
+    check_draft(shifted, run_draft(shifted))
+    rp = torch.tensor([0, 5, 12], dtype=torch.int32, device=DEV)
+    tok = torch.argmax(shifted.float(), dim=1).to(torch.int32)
+    res = binding.verify_accept(shifted, rp, tok)
+    torch.cuda.synchronize()
+    check_verify(shifted, rp.cpu().numpy(), tok, res)
+
+
+def test_empty_requests_and_workspace_reuse():
+    lay = W.make_layout("high", seed=4, num_requests=40)
+    counts = lay.n_verify.copy()
+    counts[::3] = 0
+    lay.row_indptr = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    rows = int(lay.row_indptr[-1])
+    inp = W.make_logit_inputs(lay, DEV)
+    ws = binding.new_workspace(binding.verify_accept_workspace_bytes(40, rows, lay.spec.vocab), DEV)
+    first = run_verify(lay, inp, workspace=ws)
+    check_verify(inp["verify_logits"], lay.row_indptr, inp["draft_tokens"], first)
+    second = run_verify(lay, inp, workspace=ws)  # counters must have been left at zero
+    for k in first:
+        assert torch.equal(first[k], second[k]), k
+    cnt_rows = ws[:4 * rows]
+    off = (4 * rows + 255) // 256 * 256
+    cnt_reqs = ws[off:off + 4 * 40]
+    assert (cnt_rows == 0).all() and (cnt_reqs == 0).all()
+    dws = binding.new_workspace(binding.draft_confidence_workspace_bytes(rows, lay.spec.vocab), DEV)
+    a = run_draft(inp["verify_logits"], workspace=dws)
+    b = run_draft(inp["verify_logits"], workspace=dws)
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+
+
+def test_no_verify_rows_at_all():
+    rp = torch.zeros(4, dtype=torch.int32, device=DEV)
+    logits = torch.empty(0, 128, dtype=torch.bfloat16, device=DEV)
+    tok = torch.empty(0, dtype=torch.int32, device=DEV)
+    res = binding.verify_accept(logits, rp, tok)
+    torch.cuda.synchronize()
+    assert res["accept_len"].tolist() == [0, 0, 0]
+    assert res["next_token"].tolist() == [-1, -1, -1]
+    assert res["accept_entropy"].tolist() == [0.0, 0.0, 0.0]
