@@ -1,0 +1,225 @@
+#!/usr/bin/env python3
+"""Benchmark of one fused draft-verify step on one MI355X.
+
+A step is the whole hot path over one batch: hybrid-mask paged attention
+(rg_draft_verify_attention), greedy verification / acceptance
+(rg_verify_accept) and draft confidence (rg_draft_confidence).  Inputs are
+seeded synthetic tensors resident in HBM before timing starts; several
+copies of every input are rotated through the steps so that the working
+set exceeds the 256 MB Infinity Cache and the numbers are HBM numbers.
+
+Prints one JSON line.  ``value`` is the step's achieved fraction of the HBM
+roofline (algorithmic bytes of all three calls / step time / 8 TB/s), in
+percent; the attention call's TFLOP/s and GB/s and the logit passes' GB/s
+are reported beside it, and ``roofline`` covers the attention call (the
+dominant one), timed with HIP events on its stream inside the timed region.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+CACHE_DEFEAT_BYTES = 512 << 20
+
+
+def algorithmic_work(lay):
+    """Bytes and flops the step must move / do, counting only allowed
+    (query, key) pairs: K and V of every key once per request, q and out
+    once, the page table; logits once."""
+    s = lay.spec
+    D, hq, hkv = s.head_dim, s.num_q_heads, s.num_kv_heads
+    attn_bytes = attn_flops = 0
+    for r in range(lay.num_requests):
+        L, V, B = int(lay.ctx_len[r]), int(lay.n_verify[r]), int(lay.n_draft[r])
+        n, T = V + B, L + V + B
+        attn_bytes += T * hkv * D * 2 * 2 + n * hq * D * 2 * 2 + math.ceil(T / 16) * 4 + n * hq * 4
+        attn_flops += 4 * D * hq * (V * L + V * (V + 1) // 2 + B * T)
+    rows_v, rows_d = lay.total_verify_rows, lay.total_draft_rows
+    verify_bytes = rows_v * s.vocab * 2 + rows_v * (4 + 4 + 4 + 4) + lay.num_requests * 12
+    draft_bytes = rows_d * s.vocab * 2 + rows_d * 6 * 4
+    return dict(attn_bytes=attn_bytes, attn_flops=attn_flops, verify_bytes=verify_bytes,
+                draft_bytes=draft_bytes)
+
+
+def cpu_baseline(lay, inputs, budget_s: float):
+    """The fp64 oracle as it stands, timed on this host for whole steps of
+    the same workload (bounded by ``budget_s`` of CPU time)."""
+    import numpy as np
+
+    import oracle
+    from paper_2609_34388_amd import workloads as W
+
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+    q, k, v = (W.bf16_bits(inputs[n]) for n in ("q", "k_cache", "v_cache"))
+    vl, dl = W.bf16_bits(inputs["verify_logits"]), W.bf16_bits(inputs["draft_logits"])
+    tok = inputs["draft_tokens"].cpu().numpy()
+    runs, t_total = 0, 0.0
+    while runs == 0 or (t_total < budget_s and runs < 50):
+        t0 = time.perf_counter()
+        oracle.oracle_attention(q, k, v, lay.q_indptr, lay.n_verify, lay.ctx_len, lay.page_indptr,
+                                lay.page_indices)
+        oracle.oracle_accept(vl, lay.row_indptr, tok)
+        oracle.oracle_confidence(dl)
+        t_total += time.perf_counter() - t0
+        runs += 1
+    return t_total / runs, runs, blas_threads, len(os.sched_getaffinity(0))
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="low",
+                    help="tiny | low | low_sigma2 | mid | high | long (default: low, C = 1, B = 16)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copies", type=int, default=0, help="input copies rotated (0 = enough for 512 MB)")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(requests and KV heads shard with no exchange; see DESIGN.md).", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2609_34388_amd import binding
+    from paper_2609_34388_amd import workloads as W
+
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2609_34388_amd import build_lib
+        build_lib.build()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    lay = W.make_layout(args.workload, seed=args.seed)
+    s = lay.spec
+    base = W.make_attention_inputs(lay, dev)
+    base.update(W.make_logit_inputs(lay, dev))
+    per_copy = sum(t.numel() * t.element_size() for t in base.values())
+    copies = args.copies or max(1, math.ceil(CACHE_DEFEAT_BYTES / per_copy))
+    sets = [base] + [{k: t.clone() for k, t in base.items()} for _ in range(copies - 1)]
+    page_idx = torch.as_tensor(lay.page_indices, device=dev)
+    row_indptr = torch.as_tensor(lay.row_indptr, device=dev)
+
+    layouts = [binding.make_layout(c["q"], c["k_cache"], lay.q_indptr, lay.n_verify, lay.ctx_len,
+                                   lay.page_indptr, page_idx) for c in sets]
+    attn_ws = torch.empty(max(16, binding.attention_workspace_bytes(layouts[0])), dtype=torch.uint8, device=dev)
+    ver_ws = binding.new_workspace(binding.verify_accept_workspace_bytes(
+        lay.num_requests, lay.total_verify_rows, s.vocab), dev)
+    dr_ws = binding.new_workspace(binding.draft_confidence_workspace_bytes(lay.total_draft_rows, s.vocab), dev)
+    out = torch.empty_like(base["q"])
+    lse = torch.empty(base["q"].shape[0], s.num_q_heads, dtype=torch.float32, device=dev)
+    vout = dict(row_argmax=torch.empty(lay.total_verify_rows, dtype=torch.int32, device=dev),
+                accept_len=torch.empty(lay.num_requests, dtype=torch.int32, device=dev),
+                next_token=torch.empty(lay.num_requests, dtype=torch.int32, device=dev),
+                row_entropy=torch.empty(lay.total_verify_rows, dtype=torch.float32, device=dev),
+                accept_entropy=torch.empty(lay.num_requests, dtype=torch.float32, device=dev))
+    dout = {k: torch.empty(lay.total_draft_rows, dtype=dt, device=dev)
+            for k, dt in (("top1", torch.int32), ("top2", torch.int32), ("p1", torch.float32),
+                          ("p2", torch.float32), ("margin", torch.float32), ("entropy", torch.float32))}
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        c = sets[i % copies]
+        if ev is not None:
+            ev[0].record(stream)
+        binding.draft_verify_attention(c["q"], c["k_cache"], c["v_cache"], None, None, None, None, page_idx,
+                                       out=out, lse=lse, workspace=attn_ws, layout=layouts[i % copies])
+        if ev is not None:
+            ev[1].record(stream)
+        binding.verify_accept(c["verify_logits"], row_indptr, c["draft_tokens"], workspace=ver_ws, out=vout)
+        if ev is not None:
+            ev[2].record(stream)
+        binding.draft_confidence(c["draft_logits"], workspace=dr_ws, out=dout)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    attn_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    ver_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+    dr_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
+
+    work = algorithmic_work(lay)
+    step_bytes = work["attn_bytes"] + work["verify_bytes"] + work["draft_bytes"]
+    step_gbps = step_bytes / (ms_step * 1e-3) / 1e9
+    attn_gbps = work["attn_bytes"] / (attn_ms * 1e-3) / 1e9
+    attn_tflops = work["attn_flops"] / (attn_ms * 1e-3) / 1e12
+    plan = binding.attention_plan(layouts[0])
+
+    result = {
+        "metric": "draft-verify attention TFLOP/s + logits GB/s, % of MI355X roofline, 1 GPU",
+        "value": round(100.0 * step_gbps / HBM_PEAK_GBPS, 3),
+        "unit": "% of MI355X HBM roofline (whole step: attention + verify + draft bytes / step time / 8 TB/s)",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "requests": lay.num_requests, "q_heads": s.num_q_heads,
+                   "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "page_size": 16,
+                   "context_tokens": int(lay.ctx_len.sum()), "verify_rows": int(lay.n_verify.sum()),
+                   "draft_rows": int(lay.n_draft.sum()), "vocab": s.vocab, "seed": args.seed,
+                   "input_copies_rotated": copies, "attn_chunk_keys": plan["chunk_keys"],
+                   "attn_work_items": plan["work_items"]},
+        "attention": {"ms": round(attn_ms, 5), "tflops": round(attn_tflops, 3), "gbps": round(attn_gbps, 1),
+                      "bytes": work["attn_bytes"], "flops": work["attn_flops"],
+                      "frac_hbm": round(attn_gbps / HBM_PEAK_GBPS, 4),
+                      "frac_mfma_bf16": round(attn_tflops / BF16_PEAK_TFLOPS, 5)},
+        "verify_accept": {"ms": round(ver_ms, 5), "bytes": work["verify_bytes"],
+                          "gbps": round(work["verify_bytes"] / (ver_ms * 1e-3) / 1e9, 1)},
+        "draft_confidence": {"ms": round(dr_ms, 5), "bytes": work["draft_bytes"],
+                             "gbps": round(work["draft_bytes"] / (dr_ms * 1e-3) / 1e9, 1)},
+        "logits_gbps": round((work["verify_bytes"] + work["draft_bytes"]) / ((ver_ms + dr_ms) * 1e-3) / 1e9, 1),
+        "roofline": {"kernel": "rg_draft_verify_attention (attn_fwd_kernel + attn_combine_kernel)",
+                     "bound": "hbm", "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(attn_gbps / HBM_PEAK_GBPS, 4), "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        host = {k: base[k] for k in ("q", "k_cache", "v_cache", "verify_logits", "draft_logits", "draft_tokens")}
+        sec, runs, threads, cores = cpu_baseline(lay, host, args.cpu_budget)
+        cpu_gbps = step_bytes / sec / 1e9
+        result["cpu_baseline"] = {"value": round(100.0 * cpu_gbps / HBM_PEAK_GBPS, 6),
+                                  "unit": result["unit"], "cores": threads, "kind": "oracle",
+                                  "ms_per_step": round(sec * 1e3, 2), "visible_cores": cores,
+                                  "sample": f"{runs} whole step(s) of the same workload (all requests, heads "
+                                            f"and rows), fp64 numpy oracle, mean time per step"}
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -33,11 +33,9 @@
  *   valid once the stream reaches that point.  A failed launch returns
  *   RG_ERR_HIP.
  * - Workspaces: size them with the matching *_workspace query (same
- *   arguments).  The logit entry points keep completion counters in their
- *   workspace: it must hold zeros before its first use (a zero-filled
- *   allocation, or rg_workspace_zero), and every completed call leaves those
- *   counters at zero again, so it can be reused without clearing.  Two calls
- *   in flight at once must not share a workspace.
+ *   arguments).  Their contents need no initialisation and are meaningless
+ *   after the call.  Two calls in flight at once must not share a
+ *   workspace.
  * - Inputs must be finite.
  */
 #ifndef RECGUIDE_H
@@ -119,7 +117,7 @@ rg_status rg_draft_verify_attention_workspace(const rg_attn_layout* layout, size
  *   lse   DEVICE [q_indptr[R]][Hq] fp32 natural-log log-sum-exp of the
  *         scaled, masked scores, or NULL
  *   ws    DEVICE workspace of at least the queried size (may be NULL when
- *         that size is 0); its contents need no initialisation.
+ *         that size is 0).
  */
 rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t* q,
                                     const uint16_t* k_cache, const uint16_t* v_cache,
@@ -184,10 +182,6 @@ rg_status rg_draft_confidence(const uint16_t* logits, int64_t row_stride, int32_
                               int32_t total_rows, int32_t* top1, int32_t* top2, float* p1,
                               float* p2, float* margin, float* entropy, void* ws,
                               size_t ws_bytes, void* stream);
-
-/* Zero-fill `bytes` bytes of device memory at `ws` on `stream` with a
- * kernel (no memset node), e.g. a fresh workspace before its first use. */
-rg_status rg_workspace_zero(void* ws, size_t bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -51,7 +51,7 @@ class AttnPlanInfo(ctypes.Structure):
 EXPORTS = ("rg_abi_version", "rg_status_string", "rg_draft_verify_attention_workspace",
            "rg_draft_verify_attention", "rg_draft_verify_attention_plan",
            "rg_verify_accept_workspace", "rg_verify_accept", "rg_draft_confidence_workspace",
-           "rg_draft_confidence", "rg_workspace_zero")
+           "rg_draft_confidence")
 
 _LIB = None
 
@@ -74,7 +74,6 @@ def _lib():
         "rg_verify_accept": (I32, [P, I64, I32, I32, I32, P, P, P, P, P, P, P, P, SZ, P]),
         "rg_draft_confidence_workspace": (I32, [I32, I32, ctypes.POINTER(SZ)]),
         "rg_draft_confidence": (I32, [P, I64, I32, I32, P, P, P, P, P, P, P, SZ, P]),
-        "rg_workspace_zero": (I32, [P, SZ, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -231,8 +230,8 @@ def draft_confidence_workspace_bytes(total_rows: int, vocab: int) -> int:
 
 
 def new_workspace(nbytes: int, device) -> torch.Tensor:
-    """A zero-filled workspace (the logit entry points need zeros on first use)."""
-    return torch.zeros(max(int(nbytes), 16), dtype=torch.uint8, device=device)
+    """A workspace of at least `nbytes` bytes (contents need no initialisation)."""
+    return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)
 
 
 def verify_accept(logits: torch.Tensor, row_indptr: torch.Tensor, draft_tokens: torch.Tensor, *,
@@ -291,8 +290,3 @@ def draft_confidence(logits: torch.Tensor, *, workspace: Optional[torch.Tensor] 
         _ptr(o.get("entropy")), workspace.data_ptr(), workspace.numel(), _stream(stream))
     _check(st, "rg_draft_confidence")
     return o
-
-
-def workspace_zero(ws: torch.Tensor, stream=None) -> None:
-    _check(_lib().rg_workspace_zero(ws.data_ptr(), ws.numel() * ws.element_size(), _stream(stream)),
-           "rg_workspace_zero")

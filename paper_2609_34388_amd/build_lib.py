@@ -20,8 +20,11 @@ BUILD_DIR = os.path.join(HERE, "_build")
 SOURCES = ("api.cpp", "attention.hip", "logits.hip")
 ARCH = "gfx950"
 
-# Packed fp32 VALU instructions are kept out of the generated code.
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Packed fp32 VALU instructions are kept out of the generated code; MFMA
+# accumulators are kept in architectural VGPRs (no AGPR round trips for the
+# softmax updates that touch them).
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-mfma-vgpr-form"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
           "-Wall", "-Wno-unused-function"]
 

@@ -139,15 +139,13 @@ rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
   return RG_OK;
 }
 
-size_t verify_ws_bytes(int32_t R, int32_t rows, int32_t vocab) {
-  const size_t nchunk = logit_chunks(vocab);
-  return align256((size_t)rows * 4) + align256((size_t)R * 4) + align256((size_t)rows * nchunk * 16) +
-         align256((size_t)rows * 8);
+size_t verify_ws_bytes(int32_t rows, int32_t vocab) {
+  return align256((size_t)rows * logit_chunks(vocab) * 16);
 }
 
 size_t draft_ws_bytes(int32_t rows, int32_t vocab) {
   const size_t nchunk = logit_chunks(vocab);
-  return align256((size_t)rows * 4) + align256((size_t)rows * nchunk * 16) + align256((size_t)rows * nchunk * 8);
+  return align256((size_t)rows * nchunk * 16) + align256((size_t)rows * nchunk * 8);
 }
 
 }  // namespace
@@ -235,7 +233,7 @@ rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t
 rg_status rg_verify_accept_workspace(int32_t num_requests, int32_t total_rows, int32_t vocab, size_t* bytes) {
   if (bytes == nullptr) return RG_ERR_NULL;
   if (num_requests < 1 || total_rows < 0 || vocab < 1) return RG_ERR_SHAPE;
-  *bytes = verify_ws_bytes(num_requests, total_rows, vocab);
+  *bytes = verify_ws_bytes(total_rows, vocab);
   return RG_OK;
 }
 
@@ -249,8 +247,8 @@ rg_status rg_verify_accept(const uint16_t* logits, int64_t row_stride, int32_t v
   if (total_rows > 0 && (!logits || !draft_tokens || !row_argmax)) return RG_ERR_NULL;
   if (row_stride < vocab) return RG_ERR_SHAPE;
   if ((int64_t)total_rows * logit_chunks(vocab) > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
-  const size_t need = verify_ws_bytes(num_requests, total_rows, vocab);
-  if (ws == nullptr || ws_bytes < need || !aligned(ws, 16)) return RG_ERR_WORKSPACE;
+  const size_t need = verify_ws_bytes(total_rows, vocab);
+  if (total_rows > 0 && (ws == nullptr || ws_bytes < need || !aligned(ws, 16))) return RG_ERR_WORKSPACE;
 
   VerifyArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -267,14 +265,7 @@ rg_status rg_verify_accept(const uint16_t* logits, int64_t row_stride, int32_t v
   a.next_token = next_token;
   a.row_entropy = row_entropy;
   a.accept_entropy = accept_entropy;
-  char* w = static_cast<char*>(ws);
-  a.row_cnt = reinterpret_cast<int32_t*>(w);
-  w += align256((size_t)total_rows * 4);
-  a.req_cnt = reinterpret_cast<int32_t*>(w);
-  w += align256((size_t)num_requests * 4);
-  a.chunk_st = reinterpret_cast<float4*>(w);
-  w += align256((size_t)total_rows * a.nchunk * 16);
-  a.row_st = reinterpret_cast<float2*>(w);
+  a.chunk_st = static_cast<float4*>(ws);
   a.vec = (aligned(logits, 16) && row_stride % 8 == 0) ? 1 : 0;
   a.grid_rows = (int32_t)round_up((int64_t)total_rows * a.nchunk, 8);
   return launch_verify(a, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
@@ -313,8 +304,6 @@ rg_status rg_draft_confidence(const uint16_t* logits, int64_t row_stride, int32_
   a.margin = margin;
   a.entropy = entropy;
   char* w = static_cast<char*>(ws);
-  a.row_cnt = reinterpret_cast<int32_t*>(w);
-  w += align256((size_t)total_rows * 4);
   a.chunk_a = reinterpret_cast<float4*>(w);
   w += align256((size_t)total_rows * a.nchunk * 16);
   a.chunk_b = reinterpret_cast<float2*>(w);
@@ -323,10 +312,5 @@ rg_status rg_draft_confidence(const uint16_t* logits, int64_t row_stride, int32_
   return launch_draft(a, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
 }
 
-rg_status rg_workspace_zero(void* ws, size_t bytes, void* stream) {
-  if (bytes == 0) return RG_OK;
-  if (ws == nullptr) return RG_ERR_NULL;
-  return launch_zero(ws, bytes, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
-}
 
 }  // extern "C"

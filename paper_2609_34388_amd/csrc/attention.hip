@@ -73,17 +73,48 @@ __device__ __forceinline__ int xcd_item(int grid_items) {
   return (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
 }
 
-template <int D, int QTW>
-__global__ __launch_bounds__(kAttnThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan p) {
+// Direct global -> LDS copy of 16 bytes per lane (LDS-DMA).  The wave's 64
+// lanes fill 1 KiB of LDS starting at `lds_byte_addr` (lane L at +16 L).
+// Issued through inline assembly so that the compiler does not insert a
+// wait for every outstanding copy before each LDS read; the kernel waits on
+// the vector-memory counter itself.  m0 is saved and restored around it.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_byte_addr) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(__builtin_amdgcn_readfirstlane(lds_byte_addr)), "v"(gptr)
+      : "memory");
+}
+
+// Wait until at most n vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+constexpr int kStages = 4;  // LDS ring depth (key tiles in flight: kStages - 1)
+
+template <int D, int W>
+__global__ __launch_bounds__(64 * W) void attn_fwd_kernel(AttnArgs a, AttnPlan p) {
+  constexpr int NT = 64 * W;          // threads
   constexpr int NCH = D / 8;          // 16-byte chunks per K row
   constexpr int KSTEPS = D / 16;      // MFMA k-steps of q.k
   constexpr int DT = D / 32;          // 32-wide head-dim tiles of the output
   constexpr int TILE = kKeyTile * D;  // bf16 elements of one staged K (or V) tile
-  constexpr int PER_THREAD = TILE / 8 / kAttnThreads;  // 16-byte chunks per thread
+  constexpr int BLOCKS = TILE * 2 / 1024;  // 1 KiB DMA blocks per K (or V) tile
+  constexpr int KPB = 1024 / (2 * D);      // keys per K block
+  constexpr int VBPP = D / 32;             // V blocks per page
+  constexpr int G = 2 * BLOCKS / W;        // DMA instructions per wave per tile
   constexpr int MAXPAGES = kMaxChunkKeys / kPageSize;
+  static_assert(2 * BLOCKS % W == 0, "DMA blocks must split evenly over waves");
 
-  __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][TILE];
-  __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][TILE];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_k[kStages][TILE];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_v[kStages][TILE];
   __shared__ int32_t lds_pages[MAXPAGES];
 
   const int item = xcd_item(p.grid_items);
@@ -93,7 +124,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_fwd_kernel(AttnArgs a, Attn
   const int n = rq.nv & 0xffff, nver = rq.nv >> 16, L = rq.ctx, T = L + n;
   const int g = a.g;
   const int M = n * g;
-  const int cols_per_group = 128 * QTW;
+  const int cols_per_group = 32 * W;
   const int ncg = (M + cols_per_group - 1) / cols_per_group;
   const int nch = (T + p.chunk - 1) / p.chunk;
   int local = item - rq.item_start;
@@ -107,220 +138,187 @@ __global__ __launch_bounds__(kAttnThreads) void attn_fwd_kernel(AttnArgs a, Attn
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int lc = lane & 31, lh = lane >> 5;
 
-  // Page indices of this chunk -> LDS (one round trip before the KV stream).
-  const int pg0 = kbeg / kPageSize;
-  const int npg = (kend + kPageSize - 1) / kPageSize - pg0;
-  for (int i = tid; i < npg; i += kAttnThreads) lds_pages[i] = a.page_indices[rq.page_start + pg0 + i];
-
-  // Query columns of this wave: col = token * g + head-in-group.
-  bf16x8 qf[QTW][KSTEPS];
-  int lim[QTW];
-  bool tile_on[QTW];
-  int wave_min_lim = kend;
-  for (int qt = 0; qt < QTW; ++qt) {
-    const int col0 = cg * cols_per_group + (wave + 4 * qt) * 32;
-    tile_on[qt] = col0 < M;
-    const int col = col0 + lc;
-    const bool valid = col < M;
-    const int tok = valid ? col / g : 0;
-    const int hh = col - tok * g;
-    lim[qt] = valid ? min(kend, tok < nver ? L + tok + 1 : T) : 0;
-    if (valid) wave_min_lim = min(wave_min_lim, lim[qt]);
+  // This wave's 32 query columns: col = token * g + head-in-group.
+  const int col0 = cg * cols_per_group + wave * 32;
+  const bool tile_on = col0 < M;  // wave-uniform
+  const int col = col0 + lc;
+  const bool valid = col < M;
+  const int tok = valid ? col / g : 0;
+  const int hh = col - tok * g;
+  const int lim = valid ? min(kend, tok < nver ? L + tok + 1 : T) : 0;
+  bf16x8 qf[KSTEPS];
+  {
     const uint16_t* qrow = a.q + ((size_t)(rq.q_start + tok) * a.hq + hk * g + hh) * D;
     for (int s = 0; s < KSTEPS; ++s) {
       u32x4 w = {0u, 0u, 0u, 0u};
       if (valid) w = *(const u32x4*)(qrow + s * 16 + 8 * lh);
-      qf[qt][s] = __builtin_bit_cast(bf16x8, w);
+      qf[s] = __builtin_bit_cast(bf16x8, w);
     }
   }
-  // Smallest visibility limit over the wave's valid columns (wave-uniform).
+  int wave_min_lim = valid ? lim : kend;
   for (int off = 32; off >= 1; off >>= 1) wave_min_lim = min(wave_min_lim, __shfl_xor(wave_min_lim, off));
 
-  f32x16 acc[QTW][DT];
-  float m_run[QTW], l_run[QTW];
-  for (int qt = 0; qt < QTW; ++qt) {
-    m_run[qt] = kNegInf;
-    l_run[qt] = 0.f;
-    for (int dt = 0; dt < DT; ++dt)
-      for (int i = 0; i < 16; ++i) acc[qt][dt][i] = 0.f;
-  }
-
-  __syncthreads();  // lds_pages ready
-
-  u32x4 kst[PER_THREAD], vst[PER_THREAD];
-  const size_t head_stride = (size_t)kPageSize * D;  // elements per (page, head)
-
-  auto load_tile = [&](int k0) {
-#pragma unroll
-    for (int u = 0; u < PER_THREAD; ++u) {
-      const int id = u * kAttnThreads + tid;
-      // K: chunk id -> key kk, 16-byte chunk ch of that key's row
-      {
-        const int kk = id / NCH, ch = id % NCH;
-        const int key = k0 + kk;
-        u32x4 w = {0u, 0u, 0u, 0u};
-        if (key < kend) {
-          const int page = lds_pages[key / kPageSize - pg0];
-          const uint16_t* src = a.k_cache + ((size_t)page * a.hkv + hk) * head_stride +
-                                (size_t)(key % kPageSize) * D + ch * 8;
-          w = *(const u32x4*)src;
-        }
-        kst[u] = w;
-      }
-      // V: chunk id -> page pp of the tile, head dim d, half (keys 8*half..+7)
-      {
-        const int pp = id / (2 * D), rem = id % (2 * D);
-        const int d = rem >> 1, half = rem & 1;
-        const int key = k0 + pp * kPageSize + half * 8;
-        u32x4 w = {0u, 0u, 0u, 0u};
-        if (key < kend) {
-          const int page = lds_pages[key / kPageSize - pg0];
-          const uint16_t* src = a.v_cache + ((size_t)page * a.hkv + hk) * head_stride +
-                                (size_t)d * kPageSize + half * 8;
-          w = *(const u32x4*)src;
-          const int valid = kend - key;  // keys of this 8-key run inside the chunk
-          if (valid < 8) {
-            for (int e = 0; e < 4; ++e) {
-              const int k2 = 2 * e;
-              uint32_t keep = (k2 < valid ? 0x0000ffffu : 0u) | (k2 + 1 < valid ? 0xffff0000u : 0u);
-              w[e] &= keep;
-            }
-          }
-        }
-        vst[u] = w;
-      }
-    }
-  };
-
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < PER_THREAD; ++u) {
-      const int id = u * kAttnThreads + tid;
-      {
-        const int kk = id / NCH, ch = id % NCH;
-        const int phys = ch ^ (swap23(kk & 31) & (NCH - 1));
-        *(u32x4*)(&lds_k[buf][kk * D + phys * 8]) = kst[u];
-      }
-      {
-        const int pp = id / (2 * D), rem = id % (2 * D);
-        const int d = rem >> 1, half = rem & 1;
-        *(u32x4*)(&lds_v[buf][pp * (D * kPageSize) + d * kPageSize + ((half ^ vswz(d)) * 8)]) = vst[u];
-      }
-    }
-  };
-
-  const int ntiles = (kend - kbeg + kKeyTile - 1) / kKeyTile;
-  load_tile(kbeg);
-  store_tile(0);
+  // Page indices of this chunk -> LDS (the one dependent round trip before the KV stream).
+  const int pg0 = kbeg / kPageSize;
+  const int npg = (kend + kPageSize - 1) / kPageSize - pg0;
+  for (int i = tid; i < npg; i += NT) lds_pages[i] = a.page_indices[rq.page_start + pg0 + i];
   __syncthreads();
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int k0 = kbeg + t * kKeyTile;
-    const int buf = t & 1;
-    if (t + 1 < ntiles) load_tile(k0 + kKeyTile);
+  const size_t head_stride = (size_t)kPageSize * D;  // elements per (page, head)
+  const uint16_t* kbase_g = a.k_cache + (size_t)hk * head_stride;
+  const uint16_t* vbase_g = a.v_cache + (size_t)hk * head_stride;
+  const size_t page_stride = (size_t)a.hkv * head_stride;
+  const int last_key = kend - 1;
 
-    const bool need_mask = k0 + kKeyTile > wave_min_lim;
-    f32x16 s[QTW][2];
+  // Issue the DMA of key tile `t` into ring stage t % kStages.  Keys past the
+  // chunk end read the chunk's last key (always a valid token); their scores
+  // are masked and their values zeroed before use.
+  auto issue = [&](int t) {
+    const int k0 = kbeg + t * kKeyTile;
+    const int st = t % kStages;
+    const uint32_t kl = (uint32_t)(uintptr_t)&lds_k[st][0];
+    const uint32_t vl = (uint32_t)(uintptr_t)&lds_v[st][0];
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      for (int qt = 0; qt < QTW; ++qt)
-        for (int i = 0; i < 16; ++i) s[qt][st][i] = 0.f;
-      const int krow = 32 * st + swap23(lc);
-      const uint16_t* kbase = &lds_k[buf][krow * D];
-#pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks) {
-        const int phys = (2 * ks + lh) ^ (lc & (NCH - 1));
-        const bf16x8 kf = *(const bf16x8*)(kbase + phys * 8);
-        for (int qt = 0; qt < QTW; ++qt)
-          if (tile_on[qt]) s[qt][st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qt][ks], s[qt][st], 0, 0, 0);
+    for (int i = 0; i < G; ++i) {
+      const int b = wave + i * W;  // block 0 .. 2*BLOCKS-1 (K blocks first)
+      if (b < BLOCKS) {
+        const int kk = b * KPB + lane / NCH;
+        const int pc = lane % NCH;
+        const int ch = pc ^ (swap23(kk & 31) & (NCH - 1));
+        const int key = min(k0 + kk, last_key);
+        const int page = lds_pages[key / kPageSize - pg0];
+        dma16(kbase_g + page * page_stride + (size_t)(key % kPageSize) * D + ch * 8, kl + b * 1024);
+      } else {
+        const int vb = b - BLOCKS;
+        const int pp = vb / VBPP;
+        const int d = (vb % VBPP) * 32 + (lane >> 1);
+        const int half = (lane & 1) ^ vswz(d);
+        const int key = min(k0 + pp * kPageSize, last_key);
+        const int page = lds_pages[key / kPageSize - pg0];
+        dma16(vbase_g + page * page_stride + (size_t)d * kPageSize + half * 8, vl + vb * 1024);
       }
     }
+  };
 
+  f32x16 acc[DT];
+  for (int dt = 0; dt < DT; ++dt)
+    for (int i = 0; i < 16; ++i) acc[dt][i] = 0.f;
+  float m_run = kNegInf, l_run = 0.f;
+
+  const int ntiles = (kend - kbeg + kKeyTile - 1) / kKeyTile;
+  for (int t = 0; t < kStages - 1 && t < ntiles; ++t) issue(t);
+
+  for (int t = 0; t < ntiles; ++t) {
+    if (t + kStages - 1 < ntiles) issue(t + kStages - 1);
+    const int ahead = min(kStages - 1, ntiles - 1 - t);  // tiles issued after tile t
+    if (ahead >= 3) wait_vmcnt<3 * G>();
+    else if (ahead == 2) wait_vmcnt<2 * G>();
+    else if (ahead == 1) wait_vmcnt<G>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+
+    const int k0 = kbeg + t * kKeyTile;
+    const int st = t % kStages;
+    const int nvalid = kend - k0;
+    if (nvalid < kKeyTile) {
+      // last tile of the chunk: zero the values of keys past its end
+      for (int i = tid; i < kKeyTile * D; i += NT) {
+        const int kk = i / D, d = i % D;
+        if (kk >= nvalid) {
+          const int pp = kk / kPageSize, kp = kk % kPageSize;
+          lds_v[st][pp * (D * kPageSize) + d * kPageSize + (((kp >> 3) ^ vswz(d)) * 8) + (kp & 7)] = 0;
+        }
+      }
+      __syncthreads();
+    }
+
+    if (tile_on) {
+      const bool need_mask = k0 + kKeyTile > wave_min_lim;
+      f32x16 s[2];
 #pragma unroll
-    for (int qt = 0; qt < QTW; ++qt) {
-      if (!tile_on[qt]) continue;
+      for (int sub = 0; sub < 2; ++sub) {
+        for (int i = 0; i < 16; ++i) s[sub][i] = 0.f;
+        const int krow = 32 * sub + swap23(lc);
+        const uint16_t* kb = &lds_k[st][krow * D];
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks) {
+          const int phys = (2 * ks + lh) ^ (lc & (NCH - 1));
+          const bf16x8 kf = *(const bf16x8*)(kb + phys * 8);
+          s[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[sub], 0, 0, 0);
+        }
+      }
       if (need_mask) {
-        for (int st = 0; st < 2; ++st)
+        for (int sub = 0; sub < 2; ++sub)
           for (int i = 0; i < 16; ++i) {
-            const int key = k0 + 32 * st + 16 * (i >> 3) + 8 * lh + 4 * ((i >> 2) & 1) + (i & 3);
-            if (key >= lim[qt]) s[qt][st][i] = kNegInf;
+            const int key = k0 + 32 * sub + 16 * (i >> 3) + 8 * lh + 4 * ((i >> 2) & 1) + (i & 3);
+            if (key >= lim) s[sub][i] = kNegInf;
           }
       }
       float mx = kNegInf;
-      for (int st = 0; st < 2; ++st)
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[qt][st][i]);
+      for (int sub = 0; sub < 2; ++sub)
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[sub][i]);
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[qt], mx);
-      const bool grew = m_new > m_run[qt];
+      const float m_new = fmaxf(m_run, mx);
+      const bool grew = m_new > m_run;
       if (__any(grew)) {
-        const float alpha = grew ? __builtin_amdgcn_exp2f((m_run[qt] - m_new) * a.scale_log2) : 1.f;
-        l_run[qt] *= alpha;
+        const float alpha = grew ? __builtin_amdgcn_exp2f((m_run - m_new) * a.scale_log2) : 1.f;
+        l_run *= alpha;
         for (int dt = 0; dt < DT; ++dt)
-          for (int i = 0; i < 16; ++i) acc[qt][dt][i] *= alpha;
-        m_run[qt] = m_new;
+          for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
+        m_run = m_new;
       }
       const float mc = (m_new == kNegInf) ? 0.f : m_new * a.scale_log2;
       float lsum = 0.f;
-      u32x4 pk[2][2];
-      for (int st = 0; st < 2; ++st) {
-        float pv[16];
-        for (int i = 0; i < 16; ++i) {
-          pv[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qt][st][i], a.scale_log2, -mc));
-          lsum += pv[i];
-        }
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub) {
+        u32x4 pk[2];
         for (int pp = 0; pp < 2; ++pp)
-          for (int e = 0; e < 4; ++e) pk[st][pp][e] = pack_bf16x2(pv[8 * pp + 2 * e], pv[8 * pp + 2 * e + 1]);
-      }
-      l_run[qt] += lsum;
-      // O^T += V^T P^T over the two 32-key sub-tiles (two 16-key MFMA steps each)
-      for (int st = 0; st < 2; ++st)
+          for (int e = 0; e < 4; ++e) {
+            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[sub][8 * pp + 2 * e], a.scale_log2, -mc));
+            const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[sub][8 * pp + 2 * e + 1], a.scale_log2, -mc));
+            lsum += p0 + p1;
+            pk[pp][e] = pack_bf16x2(p0, p1);
+          }
+        // O^T += V^T P^T: two 16-key MFMA steps per 32-key sub-tile
         for (int pp = 0; pp < 2; ++pp) {
-          const bf16x8 pf = __builtin_bit_cast(bf16x8, pk[st][pp]);
-          const uint16_t* vpage = &lds_v[buf][(2 * st + pp) * (D * kPageSize)];
+          const bf16x8 pf = __builtin_bit_cast(bf16x8, pk[pp]);
+          const uint16_t* vpage = &lds_v[st][(2 * sub + pp) * (D * kPageSize)];
           for (int dt = 0; dt < DT; ++dt) {
             const int d = 32 * dt + lc;
             const bf16x8 vf = *(const bf16x8*)(vpage + d * kPageSize + ((lh ^ vswz(d)) * 8));
-            acc[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[qt][dt], 0, 0, 0);
+            acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[dt], 0, 0, 0);
           }
         }
+      }
+      l_run += lsum;
     }
-
-    if (t + 1 < ntiles) store_tile(buf ^ 1);
-    __syncthreads();
+    __syncthreads();  // stage st is refilled by the next iteration's DMA
   }
 
   // Epilogue: per column, combine the two half-wave sums.
-#pragma unroll
-  for (int qt = 0; qt < QTW; ++qt) {
-    if (!tile_on[qt]) continue;
-    const float l_tot = l_run[qt] + __shfl_xor(l_run[qt], 32);
-    const int col = cg * cols_per_group + (wave + 4 * qt) * 32 + lc;
-    if (col >= M) continue;
-    const int tok = col / g;
-    const int hh = col - tok * g;
-    const size_t orow = (size_t)(rq.q_start + tok) * a.hq + hk * g + hh;
-    if (nch == 1) {
-      const float inv = 1.f / l_tot;
-      uint16_t* dst = a.out + orow * D;
-      for (int dt = 0; dt < DT; ++dt)
-        for (int ib = 0; ib < 4; ++ib) {
-          u32x2 w;
-          w[0] = pack_bf16x2(acc[qt][dt][4 * ib + 0] * inv, acc[qt][dt][4 * ib + 1] * inv);
-          w[1] = pack_bf16x2(acc[qt][dt][4 * ib + 2] * inv, acc[qt][dt][4 * ib + 3] * inv);
-          *(u32x2*)(dst + 32 * dt + 8 * ib + 4 * lh) = w;
-        }
-      if (a.lse != nullptr && lh == 0) a.lse[orow] = m_run[qt] * a.sm_scale + __logf(l_tot);
-    } else {
-      const size_t pcol = (size_t)rq.part_start + ((size_t)hk * nch + c) * M + col;
-      float* dst = a.part_o + pcol * D;
-      for (int dt = 0; dt < DT; ++dt)
-        for (int ib = 0; ib < 4; ++ib) {
-          float4 w = make_float4(acc[qt][dt][4 * ib + 0], acc[qt][dt][4 * ib + 1],
-                                 acc[qt][dt][4 * ib + 2], acc[qt][dt][4 * ib + 3]);
-          *(float4*)(dst + 32 * dt + 8 * ib + 4 * lh) = w;
-        }
-      if (lh == 0) *(float2*)(a.part_ml + 2 * pcol) = make_float2(m_run[qt], l_tot);
-    }
+  if (!tile_on || !valid) return;
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const size_t orow = (size_t)(rq.q_start + tok) * a.hq + hk * g + hh;
+  if (nch == 1) {
+    const float inv = 1.f / l_tot;
+    uint16_t* dst = a.out + orow * D;
+    for (int dt = 0; dt < DT; ++dt)
+      for (int ib = 0; ib < 4; ++ib) {
+        u32x2 w;
+        w[0] = pack_bf16x2(acc[dt][4 * ib + 0] * inv, acc[dt][4 * ib + 1] * inv);
+        w[1] = pack_bf16x2(acc[dt][4 * ib + 2] * inv, acc[dt][4 * ib + 3] * inv);
+        *(u32x2*)(dst + 32 * dt + 8 * ib + 4 * lh) = w;
+      }
+    if (a.lse != nullptr && lh == 0) a.lse[orow] = m_run * a.sm_scale + __logf(l_tot);
+  } else {
+    const size_t pcol = (size_t)rq.part_start + ((size_t)hk * nch + c) * M + col;
+    float* dst = a.part_o + pcol * D;
+    for (int dt = 0; dt < DT; ++dt)
+      for (int ib = 0; ib < 4; ++ib) {
+        float4 w = make_float4(acc[dt][4 * ib + 0], acc[dt][4 * ib + 1], acc[dt][4 * ib + 2], acc[dt][4 * ib + 3]);
+        *(float4*)(dst + 32 * dt + 8 * ib + 4 * lh) = w;
+      }
+    if (lh == 0) *(float2*)(a.part_ml + 2 * pcol) = make_float2(m_run, l_tot);
   }
 }
 
@@ -371,10 +369,9 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a, AttnPlan 
   if (a.lse != nullptr && t == 0) a.lse[orow] = mmax * a.sm_scale + __logf(lsum);
 }
 
-template <int D, int QTW>
+template <int D, int W>
 hipError_t launch_impl(const AttnArgs& args, const AttnPlan& plan, hipStream_t stream) {
-  hipLaunchKernelGGL((attn_fwd_kernel<D, QTW>), dim3(plan.grid_items), dim3(kAttnThreads), 0, stream,
-                     args, plan);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, W>), dim3(plan.grid_items), dim3(64 * W), 0, stream, args, plan);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (plan.total_comb > 0) {
@@ -389,8 +386,8 @@ hipError_t launch_impl(const AttnArgs& args, const AttnPlan& plan, hipStream_t s
 hipError_t launch_attention(const AttnArgs& args, const AttnPlan& plan, int head_dim,
                             hipStream_t stream) {
   const bool wide = plan.cols_per_group > 128;
-  if (head_dim == 128) return wide ? launch_impl<128, 2>(args, plan, stream) : launch_impl<128, 1>(args, plan, stream);
-  return wide ? launch_impl<64, 2>(args, plan, stream) : launch_impl<64, 1>(args, plan, stream);
+  if (head_dim == 128) return wide ? launch_impl<128, 8>(args, plan, stream) : launch_impl<128, 4>(args, plan, stream);
+  return wide ? launch_impl<64, 8>(args, plan, stream) : launch_impl<64, 4>(args, plan, stream);
 }
 
 }  // namespace rg

@@ -74,11 +74,7 @@ struct VerifyArgs {
   int32_t* next_token;
   float* row_entropy;
   float* accept_entropy;
-  // workspace carve-up
-  int32_t* row_cnt;    // [rows]
-  int32_t* req_cnt;    // [num_req]
-  float4* chunk_st;    // [rows * nchunk] (max, bits(argmax), Z', S)
-  float2* row_st;      // [rows] (bits(argmax), entropy)
+  float4* chunk_st;    // workspace [rows * nchunk] (max, bits(argmax), Z', S)
   int32_t vec;         // 16-byte loads allowed
   int32_t grid_rows;   // row work groups (rows * nchunk rounded up to 8)
 };
@@ -93,8 +89,7 @@ struct DraftArgs {
   float* p2;
   float* margin;
   float* entropy;
-  int32_t* row_cnt;      // [rows]
-  float4* chunk_a;       // [rows * nchunk] (max, bits(i1), v2, bits(i2))
+  float4* chunk_a;       // workspace [rows * nchunk] (max, bits(i1), v2, bits(i2))
   float2* chunk_b;       // [rows * nchunk] (Z', S)
   int32_t vec;
   int32_t grid_rows;
@@ -105,6 +100,5 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream);
 hipError_t launch_draft(const DraftArgs& a, hipStream_t stream);
-hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t stream);
 
 }  // namespace rg

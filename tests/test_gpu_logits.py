@@ -128,13 +128,10 @@ def test_empty_requests_and_workspace_reuse():
     ws = binding.new_workspace(binding.verify_accept_workspace_bytes(40, rows, lay.spec.vocab), DEV)
     first = run_verify(lay, inp, workspace=ws)
     check_verify(inp["verify_logits"], lay.row_indptr, inp["draft_tokens"], first)
-    second = run_verify(lay, inp, workspace=ws)  # counters must have been left at zero
+    ws.fill_(0xFF)  # workspace contents must not matter
+    second = run_verify(lay, inp, workspace=ws)
     for k in first:
         assert torch.equal(first[k], second[k]), k
-    cnt_rows = ws[:4 * rows]
-    off = (4 * rows + 255) // 256 * 256
-    cnt_reqs = ws[off:off + 4 * 40]
-    assert (cnt_rows == 0).all() and (cnt_reqs == 0).all()
     dws = binding.new_workspace(binding.draft_confidence_workspace_bytes(rows, lay.spec.vocab), DEV)
     a = run_draft(inp["verify_logits"], workspace=dws)
     b = run_draft(inp["verify_logits"], workspace=dws)
