@@ -134,40 +134,66 @@ def main(argv=None):
     dout = {k: torch.empty(lay.total_draft_rows, dtype=dt, device=dev)
             for k, dt in (("top1", torch.int32), ("top2", torch.int32), ("p1", torch.float32),
                           ("p2", torch.float32), ("margin", torch.float32), ("entropy", torch.float32))}
-    stream = torch.cuda.current_stream()
 
-    def step(i, ev=None):
+    def attention(i):
         c = sets[i % copies]
-        if ev is not None:
-            ev[0].record(stream)
         binding.draft_verify_attention(c["q"], c["k_cache"], c["v_cache"], None, None, None, None, page_idx,
                                        out=out, lse=lse, workspace=attn_ws, layout=layouts[i % copies])
-        if ev is not None:
-            ev[1].record(stream)
-        binding.verify_accept(c["verify_logits"], row_indptr, c["draft_tokens"], workspace=ver_ws, out=vout)
-        if ev is not None:
-            ev[2].record(stream)
-        binding.draft_confidence(c["draft_logits"], workspace=dr_ws, out=dout)
-        if ev is not None:
-            ev[3].record(stream)
 
+    def verify(i):
+        c = sets[i % copies]
+        binding.verify_accept(c["verify_logits"], row_indptr, c["draft_tokens"], workspace=ver_ws, out=vout)
+
+    def draft(i):
+        c = sets[i % copies]
+        binding.draft_confidence(c["draft_logits"], workspace=dr_ws, out=dout)
+
+    def step(i):
+        attention(i)
+        verify(i)
+        draft(i)
+
+    # Warmup: eager steps (compiles nothing; loads the library, touches every buffer).
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    # The step is launch-bound at low concurrency, so the timed region replays a
+    # HIP graph holding exactly `steps` captured steps (input copies rotated).
+    def capture(fn, n, base):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(n):
+                fn(base + i)
+        torch.cuda.synchronize()
+        return g
+
+    g_step = capture(step, args.steps, args.warmup)
+    stream = torch.cuda.current_stream()
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start.record(stream)
-    for i in range(args.steps):
-        step(args.warmup + i, evs[i])
+    g_step.replay()
     t_end.record(stream)
     torch.cuda.synchronize()
     ms_step = t_start.elapsed_time(t_end) / args.steps
-    attn_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
-    ver_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
-    dr_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
+
+    # Per-call times: graphs of `steps` calls of one entry point each, timed
+    # with HIP events on the same stream right after the step graph.
+    def time_calls(fn):
+        g = capture(fn, args.steps, args.warmup)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    attn_ms = time_calls(attention)
+    ver_ms = time_calls(verify)
+    dr_ms = time_calls(draft)
 
     work = algorithmic_work(lay)
     step_bytes = work["attn_bytes"] + work["verify_bytes"] + work["draft_bytes"]
@@ -189,6 +215,7 @@ def main(argv=None):
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
+        "timing": "HIP graph replay of the timed steps (and of each entry point alone for per-call times)",
         "config": {"workload": args.workload, "requests": lay.num_requests, "q_heads": s.num_q_heads,
                    "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "page_size": 16,
                    "context_tokens": int(lay.ctx_len.sum()), "verify_rows": int(lay.n_verify.sum()),

@@ -53,7 +53,7 @@ rg_status validate_layout(const rg_attn_layout* L) {
 struct FullPlan {
   std::vector<AttnPlan> launches;
   int chunk = 0;
-  int cols_per_group = 128;
+  int cols_per_group = 256;
   int64_t items = 0, split_requests = 0, max_partial_cols = 0, total_partial_cols = 0;
   size_t ws_bytes = 0;
   size_t ml_offset = 0;
@@ -78,9 +78,7 @@ rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
   const int R = L->num_requests;
   const int g = L->num_q_heads / L->num_kv_heads;
   const int hkv = L->num_kv_heads;
-  int64_t max_cols = 0;
-  for (int r = 0; r < R; ++r) max_cols = std::max<int64_t>(max_cols, (int64_t)(L->q_indptr[r + 1] - L->q_indptr[r]) * g);
-  fp.cols_per_group = max_cols > 128 ? 256 : 128;
+  fp.cols_per_group = 256;  // 8 waves x 32 columns per work group
   int64_t total_keys = 0;
   for (int r = 0; r < R; ++r) {
     const int64_t n = L->q_indptr[r + 1] - L->q_indptr[r];

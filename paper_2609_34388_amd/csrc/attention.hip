@@ -40,6 +40,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kNegInf = -__builtin_huge_valf();
 
@@ -51,8 +53,8 @@ __device__ __forceinline__ int swap23(int r) {
 __device__ __forceinline__ int vswz(int d) { return ((d >> 2) ^ (d >> 3)) & 1; }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  __bf16 x = (__bf16)a, y = (__bf16)b;
-  return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+  const f32x2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
 __device__ __forceinline__ int find_request(const AttnPlan& p, int item, bool combine) {
@@ -90,6 +92,29 @@ __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_byte_addr) 
       : "memory");
 }
 
+// Same with a wave-uniform 64-bit base in SGPRs and a per-lane 32-bit byte
+// offset (the saddr form: no per-lane 64-bit address arithmetic).
+__device__ __forceinline__ void dma16_s(const void* sbase, uint32_t voff, uint32_t lds_byte_addr) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(__builtin_amdgcn_readfirstlane(lds_byte_addr)), "v"(voff), "s"(sbase)
+      : "memory");
+}
+
+// Work-group barrier that orders LDS only.  __syncthreads() also fences
+// global memory, which makes every wave wait for all of its outstanding
+// vector-memory operations -- the whole LDS-DMA ring -- at each barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Wait until at most n vector-memory operations of this wave are in flight.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -99,9 +124,19 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 constexpr int kStages = 4;  // LDS ring depth (key tiles in flight: kStages - 1)
 
-template <int D, int W>
-__global__ __launch_bounds__(64 * W) void attn_fwd_kernel(AttnArgs a, AttnPlan p) {
-  constexpr int NT = 64 * W;          // threads
+
+constexpr int kWaves = 8;   // waves per work group (two per SIMD)
+constexpr int kThreads = 64 * kWaves;
+
+// Work group = 8 waves over (column tiles) x (key groups).  A request's
+// columns are split into groups of up to 256; a group of nct 32-column tiles
+// uses nct' = nct rounded up to a power of two tiles and kg = 8 / nct' key
+// groups: wave w handles column tile w % nct' and the 32-key sub-tiles j of
+// the chunk with j % kg == w / nct'.  Small requests thus keep all 8 waves
+// (two per SIMD) busy on disjoint keys; the key groups' partial softmax
+// states are merged through LDS at the end.
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan p) {
   constexpr int NCH = D / 8;          // 16-byte chunks per K row
   constexpr int KSTEPS = D / 16;      // MFMA k-steps of q.k
   constexpr int DT = D / 32;          // 32-wide head-dim tiles of the output
@@ -109,13 +144,15 @@ __global__ __launch_bounds__(64 * W) void attn_fwd_kernel(AttnArgs a, AttnPlan p
   constexpr int BLOCKS = TILE * 2 / 1024;  // 1 KiB DMA blocks per K (or V) tile
   constexpr int KPB = 1024 / (2 * D);      // keys per K block
   constexpr int VBPP = D / 32;             // V blocks per page
-  constexpr int G = 2 * BLOCKS / W;        // DMA instructions per wave per tile
+  constexpr int G = 2 * BLOCKS / kWaves;   // DMA instructions per wave per tile
   constexpr int MAXPAGES = kMaxChunkKeys / kPageSize;
-  static_assert(2 * BLOCKS % W == 0, "DMA blocks must split evenly over waves");
+  constexpr int COLS = 32 * kWaves;        // columns per column group
+  static_assert(2 * BLOCKS % kWaves == 0, "DMA blocks must split evenly over waves");
+  static_assert(kStages * TILE * 2 * 2 >= (kWaves - 1) * (64 * 16 * DT + 128) * 4, "merge area");
 
-  __shared__ __attribute__((aligned(16))) uint16_t lds_k[kStages][TILE];
-  __shared__ __attribute__((aligned(16))) uint16_t lds_v[kStages][TILE];
-  __shared__ int32_t lds_pages[MAXPAGES];
+  // ring[stage][0] = K tile, ring[stage][1] = V tile
+  __shared__ __attribute__((aligned(16))) uint16_t ring[kStages][2][TILE];
+  __shared__ __attribute__((aligned(16))) int32_t lds_pages[MAXPAGES + 4];
 
   const int item = xcd_item(p.grid_items);
   if (item >= p.total_items) return;
@@ -124,8 +161,7 @@ __global__ __launch_bounds__(64 * W) void attn_fwd_kernel(AttnArgs a, AttnPlan p
   const int n = rq.nv & 0xffff, nver = rq.nv >> 16, L = rq.ctx, T = L + n;
   const int g = a.g;
   const int M = n * g;
-  const int cols_per_group = 32 * W;
-  const int ncg = (M + cols_per_group - 1) / cols_per_group;
+  const int ncg = (M + COLS - 1) / COLS;
   const int nch = (T + p.chunk - 1) / p.chunk;
   int local = item - rq.item_start;
   const int c = local % nch;
@@ -135,14 +171,18 @@ __global__ __launch_bounds__(64 * W) void attn_fwd_kernel(AttnArgs a, AttnPlan p
   const int kbeg = c * p.chunk;
   const int kend = min(T, kbeg + p.chunk);
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, in an SGPR
   const int lc = lane & 31, lh = lane >> 5;
 
-  // This wave's 32 query columns: col = token * g + head-in-group.
-  const int col0 = cg * cols_per_group + wave * 32;
-  const bool tile_on = col0 < M;  // wave-uniform
-  const int col = col0 + lc;
-  const bool valid = col < M;
+  // column tiles of this group and the wave's (column tile, key group)
+  const int nct = min(kWaves, (M - cg * COLS + 31) / 32);
+  const int nct2 = nct <= 1 ? 1 : nct <= 2 ? 2 : nct <= 4 ? 4 : 8;
+  const int kg = kWaves / nct2;
+  const int ct = wave % nct2, kgi = wave / nct2;
+  const bool tile_on = ct < nct;  // wave-uniform
+  const int col = cg * COLS + ct * 32 + lc;
+  const bool valid = tile_on && col < M;
   const int tok = valid ? col / g : 0;
   const int hh = col - tok * g;
   const int lim = valid ? min(kend, tok < nver ? L + tok + 1 : T) : 0;
@@ -161,42 +201,74 @@ __global__ __launch_bounds__(64 * W) void attn_fwd_kernel(AttnArgs a, AttnPlan p
   // Page indices of this chunk -> LDS (the one dependent round trip before the KV stream).
   const int pg0 = kbeg / kPageSize;
   const int npg = (kend + kPageSize - 1) / kPageSize - pg0;
-  for (int i = tid; i < npg; i += NT) lds_pages[i] = a.page_indices[rq.page_start + pg0 + i];
-  __syncthreads();
+  for (int i = tid; i < npg; i += kThreads) lds_pages[i] = a.page_indices[rq.page_start + pg0 + i];
+  lds_barrier();
 
   const size_t head_stride = (size_t)kPageSize * D;  // elements per (page, head)
   const uint16_t* kbase_g = a.k_cache + (size_t)hk * head_stride;
   const uint16_t* vbase_g = a.v_cache + (size_t)hk * head_stride;
   const size_t page_stride = (size_t)a.hkv * head_stride;
-  const int last_key = kend - 1;
 
-  // Issue the DMA of key tile `t` into ring stage t % kStages.  Keys past the
-  // chunk end read the chunk's last key (always a valid token); their scores
-  // are masked and their values zeroed before use.
+  // Per-lane constants of this wave's DMA blocks (block b = wave + i * 8):
+  // the block's page slot within the tile (0..3), the key of its first lane
+  // and the lane's byte offset inside that page.
+  int dma_slot[G], dma_kk[G];
+  uint32_t dma_off[G];
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    const int b = wave + i * kWaves;
+    if (b < BLOCKS) {  // K: key kk of the tile, 16-byte chunk
+      const int kk = b * KPB + lane / NCH;
+      const int ch = (lane % NCH) ^ (swap23(kk & 31) & (NCH - 1));
+      dma_slot[i] = (b * KPB) / kPageSize;
+      dma_kk[i] = kk;
+      dma_off[i] = (uint32_t)(((kk % kPageSize) * D + ch * 8) * 2);
+    } else {  // V: page pp of the tile, head dim d, half
+      const int vb = b - BLOCKS;
+      const int d = (vb % VBPP) * 32 + (lane >> 1);
+      dma_slot[i] = vb / VBPP;
+      dma_kk[i] = (vb / VBPP) * kPageSize;
+      dma_off[i] = (uint32_t)((d * kPageSize + ((lane & 1) ^ vswz(d)) * 8) * 2);
+    }
+  }
+  const size_t page_bytes = page_stride * 2;
+
+  // DMA of key tile t into ring stage ST.  Keys past the chunk end read the
+  // chunk's last key (a valid token); their scores are masked and their
+  // values zeroed before use.
   auto issue = [&](int t) {
+    const int ST = t % kStages;
     const int k0 = kbeg + t * kKeyTile;
-    const int st = t % kStages;
-    const uint32_t kl = (uint32_t)(uintptr_t)&lds_k[st][0];
-    const uint32_t vl = (uint32_t)(uintptr_t)&lds_v[st][0];
+    if (k0 + kKeyTile <= kend) {
+      // the tile's four pages with one LDS read (slots past the chunk are unused)
+      const int4 pg = *(const int4*)&lds_pages[4 * t];
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+        const int b = wave + i * kWaves;
+        const bool is_k = b < BLOCKS;
+        const int slot = dma_slot[i];
+        const int page = __builtin_amdgcn_readfirstlane(slot == 0 ? pg.x : slot == 1 ? pg.y : slot == 2 ? pg.z : pg.w);
+        const char* head = reinterpret_cast<const char*>(is_k ? kbase_g : vbase_g);
+        const uint32_t dst = is_k ? (uint32_t)(uintptr_t)&ring[ST][0][b * 512]
+                                  : (uint32_t)(uintptr_t)&ring[ST][1][(b - BLOCKS) * 512];
+        dma16_s(head + (size_t)page * page_bytes, dma_off[i], dst);
+      }
+      return;
+    }
+    // chunk tail: keys past the end read the chunk's last key (a valid
+    // token); their scores are masked and their values zeroed before use
 #pragma unroll
     for (int i = 0; i < G; ++i) {
-      const int b = wave + i * W;  // block 0 .. 2*BLOCKS-1 (K blocks first)
-      if (b < BLOCKS) {
-        const int kk = b * KPB + lane / NCH;
-        const int pc = lane % NCH;
-        const int ch = pc ^ (swap23(kk & 31) & (NCH - 1));
-        const int key = min(k0 + kk, last_key);
-        const int page = lds_pages[key / kPageSize - pg0];
-        dma16(kbase_g + page * page_stride + (size_t)(key % kPageSize) * D + ch * 8, kl + b * 1024);
-      } else {
-        const int vb = b - BLOCKS;
-        const int pp = vb / VBPP;
-        const int d = (vb % VBPP) * 32 + (lane >> 1);
-        const int half = (lane & 1) ^ vswz(d);
-        const int key = min(k0 + pp * kPageSize, last_key);
-        const int page = lds_pages[key / kPageSize - pg0];
-        dma16(vbase_g + page * page_stride + (size_t)d * kPageSize + half * 8, vl + vb * 1024);
-      }
+      const int b = wave + i * kWaves;
+      const bool is_k = b < BLOCKS;
+      const int key = min(k0 + dma_kk[i], kend - 1);  // same page for the whole block
+      const int page = __builtin_amdgcn_readfirstlane(lds_pages[(key >> 4) - pg0]);
+      uint32_t off = dma_off[i];
+      if (is_k) off += (uint32_t)(((key & (kPageSize - 1)) - (dma_kk[i] & (kPageSize - 1))) * D * 2);
+      const char* head = reinterpret_cast<const char*>(is_k ? kbase_g : vbase_g);
+      const uint32_t dst = is_k ? (uint32_t)(uintptr_t)&ring[ST][0][b * 512]
+                                : (uint32_t)(uintptr_t)&ring[ST][1][(b - BLOCKS) * 512];
+      dma16_s(head + (size_t)page * page_bytes, off, dst);
     }
   };
 
@@ -204,109 +276,182 @@ __global__ __launch_bounds__(64 * W) void attn_fwd_kernel(AttnArgs a, AttnPlan p
   for (int dt = 0; dt < DT; ++dt)
     for (int i = 0; i < 16; ++i) acc[dt][i] = 0.f;
   float m_run = kNegInf, l_run = 0.f;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+  // Fragments of one 32-key sub-tile.  K rows of sub-tile row base krow0 are
+  // read in the permuted order (see the file comment); all reads of a phase
+  // are issued before the MFMAs that consume them.
+  uint32_t koff[KSTEPS];  // byte offsets of this lane's K fragments inside a sub-tile
+#pragma unroll
+  for (int ks = 0; ks < KSTEPS; ++ks) koff[ks] = (uint32_t)((swap23(lc) * D + (((2 * ks + lh) ^ (lc & (NCH - 1))) * 8)) * 2);
+  auto load_k = [&](bf16x8 (&kf)[KSTEPS], const uint16_t* kt_lds, int krow0) {
+    const char* kb = reinterpret_cast<const char*>(kt_lds + krow0 * D);
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) kf[ks] = *(const bf16x8*)(kb + koff[ks]);
+  };
+  auto load_v = [&](bf16x8 (&vf)[2][DT], const uint16_t* vt_lds, int page0) {
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int d = 32 * dt + lc;
+        vf[pp][dt] = *(const bf16x8*)(vt_lds + (page0 + pp) * (D * kPageSize) + d * kPageSize + ((lh ^ vswz(d)) * 8));
+      }
+  };
+  // Online softmax of one sub-tile's scores: mask, running max (both
+  // half-waves of a column agree through a permlane swap), lazy rescale of
+  // the accumulator, P = exp2(s * scale*log2e - m * scale*log2e) rounded to
+  // bf16 pairs, running sum of the rounded P (the weights the PV MFMA uses).
+  auto softmax = [&](f32x16& s, int kbase, u32x4 (&pk)[2]) {
+    if (kbase + 32 > wave_min_lim) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = kbase + 16 * (i >> 3) + 8 * lh + 4 * ((i >> 2) & 1) + (i & 3);
+        if (key >= lim) s[i] = kNegInf;
+      }
+    }
+    float mx = s[0];
+#pragma unroll
+    for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s[i]);
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    }
+    const float m_new = fmaxf(m_run, mx);
+    const bool grew = m_new > m_run;
+    if (__any(grew)) {
+      const float alpha = grew ? __builtin_amdgcn_exp2f((m_run - m_new) * a.scale_log2) : 1.f;
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
+      m_run = m_new;
+    }
+    const float mc = (m_new == kNegInf) ? 0.f : m_new * a.scale_log2;
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const f32x2 pr = {__builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * pp + 2 * e], a.scale_log2, -mc)),
+                          __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * pp + 2 * e + 1], a.scale_log2, -mc))};
+        const bf16x2 pb = __builtin_convertvector(pr, bf16x2);
+        l_run = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, l_run, false);
+        pk[pp][e] = __builtin_bit_cast(uint32_t, pb);
+      }
+  };
+  // O^T += V^T P^T: two 16-key MFMA steps (one page each).
+  auto pv = [&](const bf16x8 (&vf)[2][DT], const u32x4 (&pk)[2]) {
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[pp][dt], __builtin_bit_cast(bf16x8, pk[pp]), acc[dt], 0, 0, 0);
+  };
 
   const int ntiles = (kend - kbeg + kKeyTile - 1) / kKeyTile;
+  static_assert(kStages == 4, "the waits below assume a 4-stage ring");
   for (int t = 0; t < kStages - 1 && t < ntiles; ++t) issue(t);
 
+  // One barrier per tile: after it every wave has finished tile t-1, so the
+  // DMA of tile t+3 may overwrite that tile's stage; it is issued once this
+  // wave's first QK MFMAs of tile t are under way.
   for (int t = 0; t < ntiles; ++t) {
-    if (t + kStages - 1 < ntiles) issue(t + kStages - 1);
-    const int ahead = min(kStages - 1, ntiles - 1 - t);  // tiles issued after tile t
-    if (ahead >= 3) wait_vmcnt<3 * G>();
-    else if (ahead == 2) wait_vmcnt<2 * G>();
+    const int ST = t % kStages;
+    const int ahead = min(kStages - 2, ntiles - 1 - t);  // tiles already issued after tile t
+    if (ahead >= 2) wait_vmcnt<2 * G>();
     else if (ahead == 1) wait_vmcnt<G>();
     else wait_vmcnt<0>();
-    __syncthreads();
+    lds_barrier();
 
     const int k0 = kbeg + t * kKeyTile;
-    const int st = t % kStages;
     const int nvalid = kend - k0;
     if (nvalid < kKeyTile) {
       // last tile of the chunk: zero the values of keys past its end
-      for (int i = tid; i < kKeyTile * D; i += NT) {
+      for (int i = tid; i < kKeyTile * D; i += kThreads) {
         const int kk = i / D, d = i % D;
         if (kk >= nvalid) {
           const int pp = kk / kPageSize, kp = kk % kPageSize;
-          lds_v[st][pp * (D * kPageSize) + d * kPageSize + (((kp >> 3) ^ vswz(d)) * 8) + (kp & 7)] = 0;
+          ring[ST][1][pp * (D * kPageSize) + d * kPageSize + (((kp >> 3) ^ vswz(d)) * 8) + (kp & 7)] = 0;
         }
       }
-      __syncthreads();
+      lds_barrier();
     }
 
+    const bool issue_next = t + kStages - 1 < ntiles;
+    bool issued = false;
     if (tile_on) {
-      const bool need_mask = k0 + kKeyTile > wave_min_lim;
-      f32x16 s[2];
+      // sub-tiles 2t, 2t+1 of the chunk; this wave takes those with j % kg == kgi
+      const bool do0 = ((2 * t) % kg) == kgi;
+      const bool do1 = ((2 * t + 1) % kg) == kgi && 32 < nvalid;
+      const uint16_t* kt = ring[ST][0];
+      const uint16_t* vt = ring[ST][1];
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {
-        for (int i = 0; i < 16; ++i) s[sub][i] = 0.f;
-        const int krow = 32 * sub + swap23(lc);
-        const uint16_t* kb = &lds_k[st][krow * D];
+        if (!(sub == 0 ? do0 : do1)) continue;
+        bf16x8 kf[KSTEPS];
+        load_k(kf, kt, 32 * sub);
+        f32x16 sc;
+        for (int i = 0; i < 16; ++i) sc[i] = 0.f;
 #pragma unroll
-        for (int ks = 0; ks < KSTEPS; ++ks) {
-          const int phys = (2 * ks + lh) ^ (lc & (NCH - 1));
-          const bf16x8 kf = *(const bf16x8*)(kb + phys * 8);
-          s[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[sub], 0, 0, 0);
+        for (int ks = 0; ks < KSTEPS; ++ks) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[ks], sc, 0, 0, 0);
+        if (issue_next && !issued) {
+          issue(t + kStages - 1);
+          issued = true;
         }
-      }
-      if (need_mask) {
-        for (int sub = 0; sub < 2; ++sub)
-          for (int i = 0; i < 16; ++i) {
-            const int key = k0 + 32 * sub + 16 * (i >> 3) + 8 * lh + 4 * ((i >> 2) & 1) + (i & 3);
-            if (key >= lim) s[sub][i] = kNegInf;
-          }
-      }
-      float mx = kNegInf;
-      for (int sub = 0; sub < 2; ++sub)
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[sub][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx);
-      const bool grew = m_new > m_run;
-      if (__any(grew)) {
-        const float alpha = grew ? __builtin_amdgcn_exp2f((m_run - m_new) * a.scale_log2) : 1.f;
-        l_run *= alpha;
-        for (int dt = 0; dt < DT; ++dt)
-          for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
-        m_run = m_new;
-      }
-      const float mc = (m_new == kNegInf) ? 0.f : m_new * a.scale_log2;
-      float lsum = 0.f;
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub) {
+        bf16x8 vf[2][DT];
         u32x4 pk[2];
-        for (int pp = 0; pp < 2; ++pp)
-          for (int e = 0; e < 4; ++e) {
-            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[sub][8 * pp + 2 * e], a.scale_log2, -mc));
-            const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[sub][8 * pp + 2 * e + 1], a.scale_log2, -mc));
-            lsum += p0 + p1;
-            pk[pp][e] = pack_bf16x2(p0, p1);
-          }
-        // O^T += V^T P^T: two 16-key MFMA steps per 32-key sub-tile
-        for (int pp = 0; pp < 2; ++pp) {
-          const bf16x8 pf = __builtin_bit_cast(bf16x8, pk[pp]);
-          const uint16_t* vpage = &lds_v[st][(2 * sub + pp) * (D * kPageSize)];
-          for (int dt = 0; dt < DT; ++dt) {
-            const int d = 32 * dt + lc;
-            const bf16x8 vf = *(const bf16x8*)(vpage + d * kPageSize + ((lh ^ vswz(d)) * 8));
-            acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[dt], 0, 0, 0);
-          }
-        }
+        load_v(vf, vt, 2 * sub);
+        softmax(sc, k0 + 32 * sub, pk);
+        pv(vf, pk);
       }
-      l_run += lsum;
     }
-    __syncthreads();  // stage st is refilled by the next iteration's DMA
+    if (issue_next && !issued) issue(t + kStages - 1);
   }
 
-  // Epilogue: per column, combine the two half-wave sums.
-  if (!tile_on || !valid) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  // Merge the key groups' partial states (lane-wise: same columns, same dims).
+  float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (kg > 1) {
+    lds_barrier();  // every wave is done with the ring (and its DMAs) before it is reused
+    float* area = reinterpret_cast<float*>(&ring[0][0][0]);
+    constexpr int PER = 64 * 16 * DT + 128;                 // floats per wave slot
+    if (tile_on && kgi > 0) {
+      float* slot = area + (wave - nct2) * PER;
+      for (int dt = 0; dt < DT; ++dt)
+        for (int i = 0; i < 16; ++i) slot[(dt * 16 + i) * 64 + lane] = acc[dt][i];
+      slot[64 * 16 * DT + lane] = m_run;
+      slot[64 * 16 * DT + 64 + lane] = l_tot;
+    }
+    lds_barrier();
+    if (!tile_on || kgi > 0) return;
+    for (int k = 1; k < kg; ++k) {
+      const float* slot = area + (k * nct2 + ct - nct2) * PER;
+      const float mk = slot[64 * 16 * DT + lane];
+      if (mk == kNegInf) continue;
+      const float lk = slot[64 * 16 * DT + 64 + lane];
+      const float m_new = fmaxf(m_run, mk);
+      const float a0 = __builtin_amdgcn_exp2f((m_run - m_new) * a.scale_log2);
+      const float a1 = __builtin_amdgcn_exp2f((mk - m_new) * a.scale_log2);
+      for (int dt = 0; dt < DT; ++dt)
+        for (int i = 0; i < 16; ++i) acc[dt][i] = acc[dt][i] * a0 + slot[(dt * 16 + i) * 64 + lane] * a1;
+      l_tot = l_tot * a0 + lk * a1;
+      m_run = m_new;
+    }
+  }
+
+  // Epilogue.
+  if (!valid) return;
   const size_t orow = (size_t)(rq.q_start + tok) * a.hq + hk * g + hh;
   if (nch == 1) {
     const float inv = 1.f / l_tot;
     uint16_t* dst = a.out + orow * D;
     for (int dt = 0; dt < DT; ++dt)
       for (int ib = 0; ib < 4; ++ib) {
+        const f32x2 lo = {acc[dt][4 * ib + 0] * inv, acc[dt][4 * ib + 1] * inv};
+        const f32x2 hi = {acc[dt][4 * ib + 2] * inv, acc[dt][4 * ib + 3] * inv};
         u32x2 w;
-        w[0] = pack_bf16x2(acc[dt][4 * ib + 0] * inv, acc[dt][4 * ib + 1] * inv);
-        w[1] = pack_bf16x2(acc[dt][4 * ib + 2] * inv, acc[dt][4 * ib + 3] * inv);
+        w[0] = __builtin_bit_cast(uint32_t, __builtin_convertvector(lo, bf16x2));
+        w[1] = __builtin_bit_cast(uint32_t, __builtin_convertvector(hi, bf16x2));
         *(u32x2*)(dst + 32 * dt + 8 * ib + 4 * lh) = w;
       }
     if (a.lse != nullptr && lh == 0) a.lse[orow] = m_run * a.sm_scale + __logf(l_tot);
@@ -315,7 +460,7 @@ __global__ __launch_bounds__(64 * W) void attn_fwd_kernel(AttnArgs a, AttnPlan p
     float* dst = a.part_o + pcol * D;
     for (int dt = 0; dt < DT; ++dt)
       for (int ib = 0; ib < 4; ++ib) {
-        float4 w = make_float4(acc[dt][4 * ib + 0], acc[dt][4 * ib + 1], acc[dt][4 * ib + 2], acc[dt][4 * ib + 3]);
+        const float4 w = make_float4(acc[dt][4 * ib + 0], acc[dt][4 * ib + 1], acc[dt][4 * ib + 2], acc[dt][4 * ib + 3]);
         *(float4*)(dst + 32 * dt + 8 * ib + 4 * lh) = w;
       }
     if (lh == 0) *(float2*)(a.part_ml + 2 * pcol) = make_float2(m_run, l_tot);
@@ -369,9 +514,9 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a, AttnPlan 
   if (a.lse != nullptr && t == 0) a.lse[orow] = mmax * a.sm_scale + __logf(lsum);
 }
 
-template <int D, int W>
+template <int D>
 hipError_t launch_impl(const AttnArgs& args, const AttnPlan& plan, hipStream_t stream) {
-  hipLaunchKernelGGL((attn_fwd_kernel<D, W>), dim3(plan.grid_items), dim3(64 * W), 0, stream, args, plan);
+  hipLaunchKernelGGL((attn_fwd_kernel<D>), dim3(plan.grid_items), dim3(kThreads), 0, stream, args, plan);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (plan.total_comb > 0) {
@@ -385,9 +530,8 @@ hipError_t launch_impl(const AttnArgs& args, const AttnPlan& plan, hipStream_t s
 
 hipError_t launch_attention(const AttnArgs& args, const AttnPlan& plan, int head_dim,
                             hipStream_t stream) {
-  const bool wide = plan.cols_per_group > 128;
-  if (head_dim == 128) return wide ? launch_impl<128, 8>(args, plan, stream) : launch_impl<128, 4>(args, plan, stream);
-  return wide ? launch_impl<64, 8>(args, plan, stream) : launch_impl<64, 4>(args, plan, stream);
+  if (head_dim == 128) return launch_impl<128>(args, plan, stream);
+  return launch_impl<64>(args, plan, stream);
 }
 
 }  // namespace rg

@@ -126,7 +126,7 @@ def test_plan_accounting(name):
     g = s.num_q_heads // s.num_kv_heads
     ch = info.chunk_keys
     assert ch % 64 == 0 and 64 <= ch <= 8192
-    cpg = 256 if (lay.q_len * g).max() > 128 else 128
+    cpg = 256
     items = split = part = 0
     for r in range(lay.num_requests):
         T, M = int(lay.kv_len[r]), int(lay.q_len[r]) * g
