@@ -122,11 +122,11 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-constexpr int kStages = 4;  // LDS ring depth (key tiles in flight: kStages - 1)
-
-
-constexpr int kWaves = 8;   // waves per work group (two per SIMD)
+constexpr int kWaves = 8;    // waves per work group (two per SIMD)
 constexpr int kThreads = 64 * kWaves;
+constexpr int kSuper = 128;  // keys staged per LDS buffer (four 32-key sub-tiles)
+constexpr int kBufs = 2;     // LDS buffers: one computed, one being filled
+static_assert(kSuper % kKeyTile == 0, "a super-tile is a whole number of key tiles");
 
 // Work group = 8 waves over (column tiles) x (key groups).  A request's
 // columns are split into groups of up to 256; a group of nct 32-column tiles
@@ -135,24 +135,30 @@ constexpr int kThreads = 64 * kWaves;
 // the chunk with j % kg == w / nct'.  Small requests thus keep all 8 waves
 // (two per SIMD) busy on disjoint keys; the key groups' partial softmax
 // states are merged through LDS at the end.
+//
+// Keys stream through two LDS buffers of 128 keys (K and V of 8 pages).
+// While one buffer is computed the next one is filled by LDS-DMA; there is
+// one barrier per 128 keys, so the two waves sharing a SIMD drift out of
+// phase over their sub-tiles and one's MFMAs overlap the other's softmax.
 template <int D>
 __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan p) {
-  constexpr int NCH = D / 8;          // 16-byte chunks per K row
-  constexpr int KSTEPS = D / 16;      // MFMA k-steps of q.k
-  constexpr int DT = D / 32;          // 32-wide head-dim tiles of the output
-  constexpr int TILE = kKeyTile * D;  // bf16 elements of one staged K (or V) tile
-  constexpr int BLOCKS = TILE * 2 / 1024;  // 1 KiB DMA blocks per K (or V) tile
-  constexpr int KPB = 1024 / (2 * D);      // keys per K block
-  constexpr int VBPP = D / 32;             // V blocks per page
-  constexpr int G = 2 * BLOCKS / kWaves;   // DMA instructions per wave per tile
+  constexpr int NCH = D / 8;                   // 16-byte chunks per K row
+  constexpr int KSTEPS = D / 16;               // MFMA k-steps of q.k
+  constexpr int DT = D / 32;                   // 32-wide head-dim tiles of the output
+  constexpr int SUPER = kSuper * D;            // bf16 elements of one K (or V) buffer
+  constexpr int BLOCKS = SUPER * 2 / 1024;     // 1 KiB DMA blocks per K (or V) buffer
+  constexpr int KPB = 1024 / (2 * D);          // keys per K block
+  constexpr int VBPP = D / 32;                 // V blocks per page
+  constexpr int G = 2 * BLOCKS / kWaves;       // DMA instructions per wave per buffer
   constexpr int MAXPAGES = kMaxChunkKeys / kPageSize;
-  constexpr int COLS = 32 * kWaves;        // columns per column group
+  constexpr int COLS = 32 * kWaves;            // columns per column group
   static_assert(2 * BLOCKS % kWaves == 0, "DMA blocks must split evenly over waves");
-  static_assert(kStages * TILE * 2 * 2 >= (kWaves - 1) * (64 * 16 * DT + 128) * 4, "merge area");
+  static_assert(kBufs * SUPER * 2 * 2 >= (kWaves - 1) * (64 * 16 * DT + 128) * 4, "merge area");
 
-  // ring[stage][0] = K tile, ring[stage][1] = V tile
-  __shared__ __attribute__((aligned(16))) uint16_t ring[kStages][2][TILE];
-  __shared__ __attribute__((aligned(16))) int32_t lds_pages[MAXPAGES + 4];
+  // buf[b][0] = K of 128 keys ([key][D], 16-byte chunks swizzled per row),
+  // buf[b][1] = V of 8 pages ([page][D][16 keys], halves swizzled per row)
+  __shared__ __attribute__((aligned(16))) uint16_t buf[kBufs][2][SUPER];
+  __shared__ __attribute__((aligned(16))) int32_t lds_pages[MAXPAGES + kSuper / kPageSize];
 
   const int item = xcd_item(p.grid_items);
   if (item >= p.total_items) return;
@@ -205,70 +211,46 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   lds_barrier();
 
   const size_t head_stride = (size_t)kPageSize * D;  // elements per (page, head)
-  const uint16_t* kbase_g = a.k_cache + (size_t)hk * head_stride;
-  const uint16_t* vbase_g = a.v_cache + (size_t)hk * head_stride;
-  const size_t page_stride = (size_t)a.hkv * head_stride;
+  const char* kbase_g = reinterpret_cast<const char*>(a.k_cache + (size_t)hk * head_stride);
+  const char* vbase_g = reinterpret_cast<const char*>(a.v_cache + (size_t)hk * head_stride);
+  const size_t page_bytes = (size_t)a.hkv * head_stride * 2;
 
-  // Per-lane constants of this wave's DMA blocks (block b = wave + i * 8):
-  // the block's page slot within the tile (0..3), the key of its first lane
-  // and the lane's byte offset inside that page.
-  int dma_slot[G], dma_kk[G];
-  uint32_t dma_off[G];
-#pragma unroll
-  for (int i = 0; i < G; ++i) {
-    const int b = wave + i * kWaves;
-    if (b < BLOCKS) {  // K: key kk of the tile, 16-byte chunk
-      const int kk = b * KPB + lane / NCH;
-      const int ch = (lane % NCH) ^ (swap23(kk & 31) & (NCH - 1));
-      dma_slot[i] = (b * KPB) / kPageSize;
-      dma_kk[i] = kk;
-      dma_off[i] = (uint32_t)(((kk % kPageSize) * D + ch * 8) * 2);
-    } else {  // V: page pp of the tile, head dim d, half
-      const int vb = b - BLOCKS;
-      const int d = (vb % VBPP) * 32 + (lane >> 1);
-      dma_slot[i] = vb / VBPP;
-      dma_kk[i] = (vb / VBPP) * kPageSize;
-      dma_off[i] = (uint32_t)((d * kPageSize + ((lane & 1) ^ vswz(d)) * 8) * 2);
-    }
-  }
-  const size_t page_bytes = page_stride * 2;
+  // This wave's DMA blocks are b = wave + 8 i.  K blocks hold KPB keys each
+  // and b % 8 = wave fixes both the keys' slots within a page and their
+  // 32-key swizzle, so every K block of the wave uses the same per-lane byte
+  // offset; likewise every V block covers the same head dims (d depends on
+  // b % VBPP only).  Only the page changes from block to block.
+  static_assert((kWaves * KPB) % 32 == 0 && kWaves % VBPP == 0 && BLOCKS % VBPP == 0,
+                "per-wave DMA offsets must not depend on the block");
+  const int kk0 = wave * KPB + lane / NCH;  // key of the lane in block b, minus KPB * 8 i
+  const uint32_t off_k = (uint32_t)((((kk0 % kPageSize) * D) + (((lane % NCH) ^ (swap23(kk0 & 31) & (NCH - 1))) * 8)) * 2);
+  const int dv = (wave % VBPP) * 32 + (lane >> 1);
+  const uint32_t off_v = (uint32_t)((dv * kPageSize + ((lane & 1) ^ vswz(dv)) * 8) * 2);
 
-  // DMA of key tile t into ring stage ST.  Keys past the chunk end read the
-  // chunk's last key (a valid token); their scores are masked and their
-  // values zeroed before use.
-  auto issue = [&](int t) {
-    const int ST = t % kStages;
-    const int k0 = kbeg + t * kKeyTile;
-    if (k0 + kKeyTile <= kend) {
-      // the tile's four pages with one LDS read (slots past the chunk are unused)
-      const int4 pg = *(const int4*)&lds_pages[4 * t];
-#pragma unroll
-      for (int i = 0; i < G; ++i) {
-        const int b = wave + i * kWaves;
-        const bool is_k = b < BLOCKS;
-        const int slot = dma_slot[i];
-        const int page = __builtin_amdgcn_readfirstlane(slot == 0 ? pg.x : slot == 1 ? pg.y : slot == 2 ? pg.z : pg.w);
-        const char* head = reinterpret_cast<const char*>(is_k ? kbase_g : vbase_g);
-        const uint32_t dst = is_k ? (uint32_t)(uintptr_t)&ring[ST][0][b * 512]
-                                  : (uint32_t)(uintptr_t)&ring[ST][1][(b - BLOCKS) * 512];
-        dma16_s(head + (size_t)page * page_bytes, dma_off[i], dst);
-      }
-      return;
-    }
-    // chunk tail: keys past the end read the chunk's last key (a valid
-    // token); their scores are masked and their values zeroed before use
+  // DMA of super-tile s (keys kbeg + 128 s ...) into buffer s % 2.  Keys
+  // past the chunk end read the chunk's last key (a valid token); their
+  // scores are masked and their values zeroed before use.
+  auto issue = [&](int s) {
+    const int k0 = kbeg + s * kSuper;
+    const bool clamp = k0 + kSuper > kend;  // wave-uniform
 #pragma unroll
     for (int i = 0; i < G; ++i) {
-      const int b = wave + i * kWaves;
+      const int b = wave + i * kWaves;  // wave-uniform
       const bool is_k = b < BLOCKS;
-      const int key = min(k0 + dma_kk[i], kend - 1);  // same page for the whole block
-      const int page = __builtin_amdgcn_readfirstlane(lds_pages[(key >> 4) - pg0]);
-      uint32_t off = dma_off[i];
-      if (is_k) off += (uint32_t)(((key & (kPageSize - 1)) - (dma_kk[i] & (kPageSize - 1))) * D * 2);
-      const char* head = reinterpret_cast<const char*>(is_k ? kbase_g : vbase_g);
-      const uint32_t dst = is_k ? (uint32_t)(uintptr_t)&ring[ST][0][b * 512]
-                                : (uint32_t)(uintptr_t)&ring[ST][1][(b - BLOCKS) * 512];
-      dma16_s(head + (size_t)page * page_bytes, off, dst);
+      const int slot = is_k ? (b * KPB) / kPageSize : (b - BLOCKS) / VBPP;
+      int page;
+      uint32_t off = is_k ? off_k : off_v;
+      if (!clamp) {
+        page = lds_pages[s * (kSuper / kPageSize) + slot];
+      } else {
+        const int kk = is_k ? b * KPB + lane / NCH : slot * kPageSize;
+        const int key = min(k0 + kk, kend - 1);  // same page for the whole block
+        page = __builtin_amdgcn_readfirstlane(lds_pages[(key >> 4) - pg0]);
+        if (is_k) off += (uint32_t)(((key & (kPageSize - 1)) - (kk & (kPageSize - 1))) * D * 2);
+      }
+      const uint32_t dst = is_k ? (uint32_t)(uintptr_t)&buf[s & 1][0][b * 512]
+                                : (uint32_t)(uintptr_t)&buf[s & 1][1][(b - BLOCKS) * 512];
+      dma16_s((is_k ? kbase_g : vbase_g) + (size_t)__builtin_amdgcn_readfirstlane(page) * page_bytes, off, dst);
     }
   };
 
@@ -278,41 +260,45 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   float m_run = kNegInf, l_run = 0.f;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // Fragments of one 32-key sub-tile.  K rows of sub-tile row base krow0 are
-  // read in the permuted order (see the file comment); all reads of a phase
-  // are issued before the MFMAs that consume them.
-  uint32_t koff[KSTEPS];  // byte offsets of this lane's K fragments inside a sub-tile
+  uint32_t koff[KSTEPS];  // byte offsets of this lane's K fragments inside a 32-key sub-tile
 #pragma unroll
   for (int ks = 0; ks < KSTEPS; ++ks) koff[ks] = (uint32_t)((swap23(lc) * D + (((2 * ks + lh) ^ (lc & (NCH - 1))) * 8)) * 2);
-  auto load_k = [&](bf16x8 (&kf)[KSTEPS], const uint16_t* kt_lds, int krow0) {
-    const char* kb = reinterpret_cast<const char*>(kt_lds + krow0 * D);
+
+  // S^T of sub-tile q (keys 32 q .. 32 q + 31 of the buffer).
+  auto qk = [&](const uint16_t* kt, int q) {
+    const char* kb = reinterpret_cast<const char*>(kt + 32 * q * D);
+    bf16x8 kf[KSTEPS];
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) kf[ks] = *(const bf16x8*)(kb + koff[ks]);
+    f32x16 sc;
+    for (int i = 0; i < 16; ++i) sc[i] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[ks], sc, 0, 0, 0);
+    return sc;
   };
-  auto load_v = [&](bf16x8 (&vf)[2][DT], const uint16_t* vt_lds, int page0) {
+  // Online softmax of one sub-tile's scores (keys kbase ..): mask, running max
+  // (both half-waves of a column agree through a permlane swap), lazy rescale
+  // of the accumulator, then O^T += V^T P^T with P rounded to bf16; the
+  // running sum adds the same rounded P the MFMA uses.
+  auto softmax_pv = [&](f32x16 sc, int kbase, const uint16_t* vt, int q) {
+    if (kbase + 32 > wave_min_lim) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = kbase + 16 * (i >> 3) + 8 * lh + 4 * ((i >> 2) & 1) + (i & 3);
+        if (key >= lim) sc[i] = kNegInf;
+      }
+    }
+    bf16x8 vf[2][DT];
 #pragma unroll
     for (int pp = 0; pp < 2; ++pp)
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const int d = 32 * dt + lc;
-        vf[pp][dt] = *(const bf16x8*)(vt_lds + (page0 + pp) * (D * kPageSize) + d * kPageSize + ((lh ^ vswz(d)) * 8));
+        vf[pp][dt] = *(const bf16x8*)(vt + (2 * q + pp) * (D * kPageSize) + d * kPageSize + ((lh ^ vswz(d)) * 8));
       }
-  };
-  // Online softmax of one sub-tile's scores: mask, running max (both
-  // half-waves of a column agree through a permlane swap), lazy rescale of
-  // the accumulator, P = exp2(s * scale*log2e - m * scale*log2e) rounded to
-  // bf16 pairs, running sum of the rounded P (the weights the PV MFMA uses).
-  auto softmax = [&](f32x16& s, int kbase, u32x4 (&pk)[2]) {
-    if (kbase + 32 > wave_min_lim) {
+    float mx = sc[0];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = kbase + 16 * (i >> 3) + 8 * lh + 4 * ((i >> 2) & 1) + (i & 3);
-        if (key >= lim) s[i] = kNegInf;
-      }
-    }
-    float mx = s[0];
-#pragma unroll
-    for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s[i]);
+    for (int i = 1; i < 16; ++i) mx = fmaxf(mx, sc[i]);
     {
       const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
       mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
@@ -329,92 +315,58 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
       m_run = m_new;
     }
     const float mc = (m_new == kNegInf) ? 0.f : m_new * a.scale_log2;
+    u32x4 pk[2];
 #pragma unroll
     for (int pp = 0; pp < 2; ++pp)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const f32x2 pr = {__builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * pp + 2 * e], a.scale_log2, -mc)),
-                          __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * pp + 2 * e + 1], a.scale_log2, -mc))};
+        const f32x2 pr = {__builtin_amdgcn_exp2f(__builtin_fmaf(sc[8 * pp + 2 * e], a.scale_log2, -mc)),
+                          __builtin_amdgcn_exp2f(__builtin_fmaf(sc[8 * pp + 2 * e + 1], a.scale_log2, -mc))};
         const bf16x2 pb = __builtin_convertvector(pr, bf16x2);
         l_run = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, l_run, false);
         pk[pp][e] = __builtin_bit_cast(uint32_t, pb);
       }
-  };
-  // O^T += V^T P^T: two 16-key MFMA steps (one page each).
-  auto pv = [&](const bf16x8 (&vf)[2][DT], const u32x4 (&pk)[2]) {
 #pragma unroll
     for (int pp = 0; pp < 2; ++pp)
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
         acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[pp][dt], __builtin_bit_cast(bf16x8, pk[pp]), acc[dt], 0, 0, 0);
   };
-
-  const int ntiles = (kend - kbeg + kKeyTile - 1) / kKeyTile;
-  static_assert(kStages == 4, "the waits below assume a 4-stage ring");
-  for (int t = 0; t < kStages - 1 && t < ntiles; ++t) issue(t);
-
-  // One barrier per tile: after it every wave has finished tile t-1, so the
-  // DMA of tile t+3 may overwrite that tile's stage; it is issued once this
-  // wave's first QK MFMAs of tile t are under way.
-  for (int t = 0; t < ntiles; ++t) {
-    const int ST = t % kStages;
-    const int ahead = min(kStages - 2, ntiles - 1 - t);  // tiles already issued after tile t
-    if (ahead >= 2) wait_vmcnt<2 * G>();
-    else if (ahead == 1) wait_vmcnt<G>();
-    else wait_vmcnt<0>();
-    lds_barrier();
-
-    const int k0 = kbeg + t * kKeyTile;
+  const int nsup = (kend - kbeg + kSuper - 1) / kSuper;
+  issue(0);
+  for (int s = 0; s < nsup; ++s) {
+    wait_vmcnt<0>();  // this wave's DMA of super-tile s
+    lds_barrier();    // everyone's: buffer s % 2 is full, buffer (s + 1) % 2 is no longer read
+    const int k0 = kbeg + s * kSuper;
     const int nvalid = kend - k0;
-    if (nvalid < kKeyTile) {
-      // last tile of the chunk: zero the values of keys past its end
-      for (int i = tid; i < kKeyTile * D; i += kThreads) {
+    const uint16_t* kt = buf[s & 1][0];
+    const uint16_t* vt = buf[s & 1][1];
+    if (nvalid < kSuper) {
+      // last buffer of the chunk: zero the values of keys past its end
+      uint16_t* vz = buf[s & 1][1];
+      for (int i = tid; i < kSuper * D; i += kThreads) {
         const int kk = i / D, d = i % D;
         if (kk >= nvalid) {
           const int pp = kk / kPageSize, kp = kk % kPageSize;
-          ring[ST][1][pp * (D * kPageSize) + d * kPageSize + (((kp >> 3) ^ vswz(d)) * 8) + (kp & 7)] = 0;
+          vz[pp * (D * kPageSize) + d * kPageSize + (((kp >> 3) ^ vswz(d)) * 8) + (kp & 7)] = 0;
         }
       }
       lds_barrier();
     }
-
-    const bool issue_next = t + kStages - 1 < ntiles;
-    bool issued = false;
+    if (s + 1 < nsup) issue(s + 1);
     if (tile_on) {
-      // sub-tiles 2t, 2t+1 of the chunk; this wave takes those with j % kg == kgi
-      const bool do0 = ((2 * t) % kg) == kgi;
-      const bool do1 = ((2 * t + 1) % kg) == kgi && 32 < nvalid;
-      const uint16_t* kt = ring[ST][0];
-      const uint16_t* vt = ring[ST][1];
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub) {
-        if (!(sub == 0 ? do0 : do1)) continue;
-        bf16x8 kf[KSTEPS];
-        load_k(kf, kt, 32 * sub);
-        f32x16 sc;
-        for (int i = 0; i < 16; ++i) sc[i] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KSTEPS; ++ks) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[ks], sc, 0, 0, 0);
-        if (issue_next && !issued) {
-          issue(t + kStages - 1);
-          issued = true;
-        }
-        bf16x8 vf[2][DT];
-        u32x4 pk[2];
-        load_v(vf, vt, 2 * sub);
-        softmax(sc, k0 + 32 * sub, pk);
-        pv(vf, pk);
-      }
+      // this wave's sub-tiles of the buffer: global sub-tile j = 4 s + q with j % kg == kgi
+      for (int q = 0; q < kSuper / 32; ++q)
+        if ((4 * s + q) % kg == kgi && 32 * q < nvalid) softmax_pv(qk(kt, q), k0 + 32 * q, vt, q);
     }
-    if (issue_next && !issued) issue(t + kStages - 1);
   }
 
   // Merge the key groups' partial states (lane-wise: same columns, same dims).
   float l_tot = l_run + __shfl_xor(l_run, 32);
   if (kg > 1) {
-    lds_barrier();  // every wave is done with the ring (and its DMAs) before it is reused
-    float* area = reinterpret_cast<float*>(&ring[0][0][0]);
-    constexpr int PER = 64 * 16 * DT + 128;                 // floats per wave slot
+    lds_barrier();  // every wave is done with the buffers before they are reused
+    float* area = reinterpret_cast<float*>(&buf[0][0][0]);
+    constexpr int PER = 64 * 16 * DT + 128;  // floats per wave slot
     if (tile_on && kgi > 0) {
       float* slot = area + (wave - nct2) * PER;
       for (int dt = 0; dt < DT; ++dt)

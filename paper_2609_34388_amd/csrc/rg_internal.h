@@ -11,7 +11,7 @@ namespace rg {
 
 constexpr int kPageSize = 16;
 constexpr int kMaxReqPerLaunch = 128;  // equals RG_ATTN_MAX_REQS_PER_LAUNCH
-constexpr int kKeyTile = 64;           // keys staged in LDS per step
+constexpr int kKeyTile = 128;          // keys per LDS buffer; chunks are multiples of it
 constexpr int kMaxChunkKeys = 8192;    // keys per work item at most
 constexpr int kAttnThreads = 256;      // 4 waves of 64
 

@@ -125,7 +125,7 @@ def test_plan_accounting(name):
     info = _plan(l)
     g = s.num_q_heads // s.num_kv_heads
     ch = info.chunk_keys
-    assert ch % 64 == 0 and 64 <= ch <= 8192
+    assert ch % 128 == 0 and 128 <= ch <= 8192
     cpg = 256
     items = split = part = 0
     for r in range(lay.num_requests):
@@ -152,7 +152,7 @@ def test_plan_chunk_override_and_workspace_monotone(monkeypatch):
                     num_pages=lay.num_pages, ctx=lay.ctx_len, nv=lay.n_verify, n=lay.q_len,
                     pages=np.diff(lay.page_indptr))
     sizes = []
-    for ch in (8192, 2048, 512, 128):
+    for ch in (8192, 2048, 512, 128):  # multiples of the 128-key buffer
         monkeypatch.setenv("RG_ATTN_CHUNK", str(ch))
         info = _plan(mk())
         assert info.chunk_keys == ch

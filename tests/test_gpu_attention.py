@@ -107,15 +107,15 @@ def test_edge_cases(case):
     check(out, lse, reference(lay, inp))
 
 
-@pytest.mark.parametrize("chunk", ["64", "128", "320", "1024"])
-def test_split_kv_chunks(monkeypatch, chunk):
+@pytest.mark.parametrize("chunk,expect", [("64", 128), ("128", 128), ("320", 384), ("1024", 1024)])
+def test_split_kv_chunks(monkeypatch, chunk, expect):
     monkeypatch.setenv("RG_ATTN_CHUNK", chunk)
     lay = W.make_layout("mid", seed=4, num_requests=4, ctx=("uniform", 200, 1500))
     inp = W.make_attention_inputs(lay, DEV, poison=float("nan"))
     info = binding.attention_plan(binding.make_layout(inp["q"], inp["k_cache"], lay.q_indptr, lay.n_verify,
                                                       lay.ctx_len, lay.page_indptr,
                                                       torch.as_tensor(lay.page_indices, device=DEV)))
-    assert info["chunk_keys"] == int(chunk)
+    assert info["chunk_keys"] == expect  # forced sizes round up to whole 128-key buffers
     out, lse = run(lay, inp)
     check(out, lse, reference(lay, inp))
 
