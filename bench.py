@@ -11,8 +11,18 @@ set exceeds the 256 MB Infinity Cache and the numbers are HBM numbers.
 Prints one JSON line.  ``value`` is the step's achieved fraction of the HBM
 roofline (algorithmic bytes of all three calls / step time / 8 TB/s), in
 percent; the attention call's TFLOP/s and GB/s and the logit passes' GB/s
-are reported beside it, and ``roofline`` covers the attention call (the
-dominant one), timed with HIP events on its stream inside the timed region.
+are reported beside it.  The timed region replays a HIP graph of exactly
+``--steps`` steps between two HIP events on the capturing stream; each entry
+point is then timed the same way from a graph of ``--steps`` calls of it
+alone.  ``roofline`` covers the attention call (the dominant one): its
+algorithmic bytes over its per-call time.  ``roofline.traffic`` is the HBM
+traffic per call measured with rocprofv3 counters (FETCH_SIZE + WRITE_SIZE,
+scaled by what the same counters read for a plain copy of known size); it
+is read from the committed profile summary and reported only while the
+attention sources still hash to the ones that summary was taken with.
+
+``--copy-calibration-mb N`` instead runs a plain device-to-device copy of N
+MiB a few times (for calibrating those counters) and exits.
 """
 from __future__ import annotations
 
@@ -30,6 +40,48 @@ if ROOT not in sys.path:
 HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 CACHE_DEFEAT_BYTES = 512 << 20
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_low_traffic.md")
+ATTN_SOURCES = ("attention.hip", "rg_internal.h", "api.cpp")
+
+
+def attention_source_hash():
+    """sha256 over the sources that decide what the attention call launches."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in ATTN_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_34388_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per attention call from the committed counter summary, or
+    None when there is none for this workload or the sources changed since."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    for line in open(TRAFFIC_FILE):
+        if line.startswith("TRAFFIC_JSON "):
+            rec = json.loads(line[len("TRAFFIC_JSON "):])
+            if rec.get("workload") == workload and rec.get("source_sha256") == attention_source_hash():
+                return rec["hbm_bytes_per_call"]
+    return None
+
+
+def copy_calibration(mib):
+    import torch
+
+    n = (mib << 20) // 2
+    src = torch.ones(n, dtype=torch.bfloat16, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration": {"bytes_read_per_copy": 2 * n, "bytes_written_per_copy": 2 * n,
+                                           "copies": 3}}), flush=True)
+    return 0
 
 
 def algorithmic_work(lay):
@@ -90,12 +142,17 @@ def main(argv=None):
     ap.add_argument("--copies", type=int, default=0, help="input copies rotated (0 = enough for 512 MB)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="run a plain copy of this many MiB (counter calibration) and exit")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(requests and KV heads shard with no exchange; see DESIGN.md).", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
+              "(requests and KV heads would shard across GPUs with no exchange).", file=sys.stderr)
         return 2
+
+    if args.copy_calibration_mb > 0:
+        return copy_calibration(args.copy_calibration_mb)
 
     import torch
 
@@ -201,6 +258,7 @@ def main(argv=None):
     attn_gbps = work["attn_bytes"] / (attn_ms * 1e-3) / 1e9
     attn_tflops = work["attn_flops"] / (attn_ms * 1e-3) / 1e12
     plan = binding.attention_plan(layouts[0])
+    traffic = measured_traffic(args.workload) if args.seed == 0 else None
 
     result = {
         "metric": "draft-verify attention TFLOP/s + logits GB/s, % of MI355X roofline, 1 GPU",
@@ -233,7 +291,8 @@ def main(argv=None):
         "logits_gbps": round((work["verify_bytes"] + work["draft_bytes"]) / ((ver_ms + dr_ms) * 1e-3) / 1e9, 1),
         "roofline": {"kernel": "rg_draft_verify_attention (attn_fwd_kernel + attn_combine_kernel)",
                      "bound": "hbm", "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(attn_gbps / HBM_PEAK_GBPS, 4), "traffic": None},
+                     "frac": round(attn_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "algorithmic_bytes": work["attn_bytes"], "us_per_call": round(attn_ms * 1e3, 3)},
     }
     if not args.no_cpu_baseline:
         host = {k: base[k] for k in ("q", "k_cache", "v_cache", "verify_logits", "draft_logits", "draft_tokens")}
