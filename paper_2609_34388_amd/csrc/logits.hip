@@ -20,8 +20,9 @@
 // f = exp(m_lose - m), Z' gains f (1 + Z'_lose) and S gains
 // f (S_lose + (m_lose - m)(1 + Z'_lose)); (value, index) pairs merge by value,
 // then lower index.  The finalize kernel merges each row's chunk states in a
-// fixed order (one wave per row) and, for verify rows, one work group per
-// request scans its rows for the first mismatch.  The kernel boundary is the
+// fixed order (a group of lanes per row, all states fetched at once) and, for
+// verify rows, one work group per request scans its rows for the first
+// mismatch.  The kernel boundary is the
 // only cross-work-group synchronisation: no atomics, no device-scope fences,
 // and the workspace needs no initialisation.
 #include "rg_internal.h"
@@ -86,24 +87,38 @@ __device__ __forceinline__ void load_chunk(const uint16_t* row, int v0, int v1, 
   }
 }
 
-// Work-group reductions over 256 threads (4 waves); every thread gets the
-// result.  `red` is an LDS array private to the call site.
-__device__ __forceinline__ float wg_max(float v, float* red) {
-  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  v = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  __syncthreads();
-  return v;
+// Wave reductions: four DPP steps (xor 1, xor 2, half-row mirror, row
+// mirror) leave every lane of a 16-lane row holding that row's result; the
+// four row results are then read as scalars and combined, so every lane gets
+// the wave's result without going through LDS.
+template <int CTRL>
+__device__ __forceinline__ int dpp(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(dpp<CTRL>(__float_as_int(v)));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+
+template <typename T>
+__device__ __forceinline__ T lane_read(T v, int l) {
+  if constexpr (sizeof(T) == 4 && __is_same(T, float))
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+  else
+    return __builtin_amdgcn_readlane(v, l);
 }
 
-__device__ __forceinline__ int wg_min(int v, int* red) {
-  for (int off = 32; off >= 1; off >>= 1) v = min(v, __shfl_xor(v, off));
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  v = min(min(red[0], red[1]), min(red[2], red[3]));
-  __syncthreads();
-  return v;
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_reduce(T v, Op op) {
+  v = op(v, dpp<kDppXor1>(v));
+  v = op(v, dpp<kDppXor2>(v));
+  v = op(v, dpp<kDppHalfMirror>(v));
+  v = op(v, dpp<kDppMirror>(v));
+  return op(op(lane_read(v, 0), lane_read(v, 16)), op(lane_read(v, 32), lane_read(v, 48)));
 }
 
 // Largest and second largest value of the multiset {a1 >= a2} U {b1 >= b2}.
@@ -111,82 +126,61 @@ __device__ __forceinline__ void top2_merge(float& a1, float& a2, float b1, float
   a2 = fmaxf(fminf(a1, b1), fmaxf(a2, b2));
   a1 = fmaxf(a1, b1);
 }
-
-__device__ __forceinline__ void wg_top2(float& v1, float& v2, float* red) {
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float o1 = __shfl_xor(v1, off), o2 = __shfl_xor(v2, off);
-    top2_merge(v1, v2, o1, o2);
-  }
-  if ((threadIdx.x & 63) == 0) {
-    red[2 * (threadIdx.x >> 6)] = v1;
-    red[2 * (threadIdx.x >> 6) + 1] = v2;
-  }
-  __syncthreads();
-  v1 = red[0];
-  v2 = red[1];
-  for (int w = 1; w < 4; ++w) top2_merge(v1, v2, red[2 * w], red[2 * w + 1]);
-  __syncthreads();
+// Smallest and second smallest of two disjoint sets {a1 <= a2}, {b1 <= b2}.
+__device__ __forceinline__ void min2_merge(int& a1, int& a2, int b1, int b2) {
+  a2 = min(max(a1, b1), min(a2, b2));
+  a1 = min(a1, b1);
 }
 
-__device__ __forceinline__ void wg_sum2(float& a, float& b, float* red) {
-  for (int off = 32; off >= 1; off >>= 1) {
-    a += __shfl_xor(a, off);
-    b += __shfl_xor(b, off);
-  }
-  if ((threadIdx.x & 63) == 0) {
-    red[2 * (threadIdx.x >> 6)] = a;
-    red[2 * (threadIdx.x >> 6) + 1] = b;
-  }
-  __syncthreads();
-  a = (red[0] + red[2]) + (red[4] + red[6]);
-  b = (red[1] + red[3]) + (red[5] + red[7]);
-  __syncthreads();
+template <int CTRL>
+__device__ __forceinline__ void top2_step(float& v1, float& v2) {
+  top2_merge(v1, v2, dpp<CTRL>(v1), dpp<CTRL>(v2));
+}
+template <int CTRL>
+__device__ __forceinline__ void min2_step(int& v1, int& v2) {
+  min2_merge(v1, v2, dpp<CTRL>(v1), dpp<CTRL>(v2));
 }
 
-// Z' (sum of exp(x - m) over entries other than index `top`) and
-// sum exp(x - m) * t with t = (x - m) log2(e).  Only the wave holding `top`
-// pays for excluding it.
-template <bool TAIL>
-__device__ __forceinline__ void exp_sums(const float (&x)[kE], int v0, float m, int top, float& z, float& s) {
-  const float mc = m * kLog2e;
-  int kt = -1;  // position of `top` among this thread's entries
-  {
-    const int rel = top - v0 - (int)threadIdx.x * 8;
-    if (rel >= 0 && (rel % (kLogitThreads * 8)) < 8 && rel / (kLogitThreads * 8) < kU)
-      kt = 8 * (rel / (kLogitThreads * 8)) + rel % (kLogitThreads * 8);
-  }
-  z = 0.f;
-  s = 0.f;
-  if (__any(kt >= 0)) {
-#pragma unroll
-    for (int k = 0; k < kE; ++k) {
-      float t = __builtin_fmaf(x[k], kLog2e, -mc);
-      if (TAIL) t = fmaxf(t, -1000.f);  // entries past the row end are -inf
-      const float e = (k == kt) ? 0.f : __builtin_amdgcn_exp2f(t);
-      z += e;
-      s = __builtin_fmaf(e, t, s);
-    }
-  } else {
-#pragma unroll
-    for (int k = 0; k < kE; ++k) {
-      float t = __builtin_fmaf(x[k], kLog2e, -mc);
-      if (TAIL) t = fmaxf(t, -1000.f);
-      const float e = __builtin_amdgcn_exp2f(t);
-      z += e;
-      s = __builtin_fmaf(e, t, s);
-    }
-  }
+__device__ __forceinline__ void wave_top2(float& v1, float& v2) {
+  top2_step<kDppXor1>(v1, v2);
+  top2_step<kDppXor2>(v1, v2);
+  top2_step<kDppHalfMirror>(v1, v2);
+  top2_step<kDppMirror>(v1, v2);
+  float a1 = lane_read(v1, 0), a2 = lane_read(v2, 0);
+  for (int l = 16; l < 64; l += 16) top2_merge(a1, a2, lane_read(v1, l), lane_read(v2, l));
+  v1 = a1;
+  v2 = a2;
+}
+
+__device__ __forceinline__ void wave_min2(int& v1, int& v2) {
+  min2_step<kDppXor1>(v1, v2);
+  min2_step<kDppXor2>(v1, v2);
+  min2_step<kDppHalfMirror>(v1, v2);
+  min2_step<kDppMirror>(v1, v2);
+  int a1 = lane_read(v1, 0), a2 = lane_read(v2, 0);
+  for (int l = 16; l < 64; l += 16) min2_merge(a1, a2, lane_read(v1, l), lane_read(v2, l));
+  v1 = a1;
+  v2 = a2;
 }
 
 struct ChunkRed {
-  float f[8];
-  int i[4];
+  float top[2][4];  // per wave: largest, second largest value
+  float zs[2][4];   // per wave: Z'' and S partial sums
+  int cnt[4];       // per wave: entries equal to the chunk maximum
+  int idx[3][4];    // per wave: first, second index of the maximum; first index of the runner-up
 };
 
-// One chunk of one row -> (m, i1, v2, i2, Z', S).
+// One chunk of one row -> (m, i1, v2, i2, Z', S) in two reduction rounds.
+// Round 1: the chunk maximum m (and, for draft rows, the runner-up value v2,
+// equal to m when the maximum occurs twice).  Round 2, in one pass over the
+// registers: Z'' = sum of exp(x - m) over entries below m, S, the number of
+// entries equal to m, the two lowest indices holding m and the lowest index
+// holding v2.  Then Z' (all but the top entry) = Z'' + (count - 1), exactly.
+// Only thread 0 receives (i1, i2, Z', S).
 template <bool DRAFT>
 __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1, bool vec, ChunkRed& red,
                                             float& m, int& i1, float& v2, int& i2, float& z, float& s) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   float x[kE];
   load_chunk(row, v0, v1, vec, x);
 
@@ -196,26 +190,76 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
     if (DRAFT) a2 = fmaxf(a2, fminf(a1, x[k]));
     a1 = fmaxf(a1, x[k]);
   }
-  if (DRAFT) wg_top2(a1, a2, red.f);  // a1 = chunk max, a2 = runner-up value (== a1 on a tie)
-  else a1 = wg_max(a1, red.f);
-  m = a1;
-  int idx = kNoIndex;  // lowest index holding m
-  for (int k = 0; k < kE; ++k)
-    if (x[k] == m) { idx = entry_index(v0, k); break; }
-  i1 = wg_min(idx, red.i);
-  v2 = kNegInf;
-  i2 = kNoIndex;
-  if (DRAFT) {
-    v2 = a2;
-    int j = kNoIndex;
-    for (int k = 0; k < kE; ++k)
-      if (x[k] == v2 && entry_index(v0, k) != i1) { j = entry_index(v0, k); break; }
-    i2 = wg_min(j, red.i);
+  if (DRAFT) wave_top2(a1, a2);
+  else a1 = wave_reduce(a1, [](float p, float q) { return fmaxf(p, q); });
+  if (lane == 0) {
+    red.top[0][wave] = a1;
+    red.top[1][wave] = a2;
   }
-  if (v0 + kLogitChunk > v1) exp_sums<true>(x, v0, m, i1, z, s);
-  else exp_sums<false>(x, v0, m, i1, z, s);
-  wg_sum2(z, s, red.f);
-  s *= kLn2;
+  __syncthreads();
+  m = red.top[0][0];
+  v2 = DRAFT ? red.top[1][0] : kNegInf;
+  for (int w = 1; w < kLogitThreads / 64; ++w) {
+    if (DRAFT) top2_merge(m, v2, red.top[0][w], red.top[1][w]);
+    else m = fmaxf(m, red.top[0][w]);
+  }
+
+  const float mc = m * kLog2e;
+  const bool tail = v0 + kLogitChunk > v1;
+  float zz = 0.f, ss = 0.f;
+  int cnt = 0, f1 = kNoIndex, f2 = kNoIndex, g = kNoIndex;
+#pragma unroll
+  for (int k = kE - 1; k >= 0; --k) {  // descending, so the lowest index is assigned last
+    const bool top = x[k] == m;
+    float t = __builtin_fmaf(x[k], kLog2e, -mc);
+    if (tail) t = fmaxf(t, -1000.f);  // entries past the row end are -inf
+    const float e = top ? 0.f : __builtin_amdgcn_exp2f(t);
+    zz += e;
+    ss = __builtin_fmaf(e, t, ss);
+    cnt += top ? 1 : 0;
+    const int idx = entry_index(v0, k);
+    if (top) {
+      f2 = f1;
+      f1 = idx;
+    }
+    if (DRAFT && x[k] == v2 && v2 != kNegInf) g = idx;
+  }
+  const auto add = [](float p, float q) { return p + q; };
+  zz = wave_reduce(zz, add);
+  ss = wave_reduce(ss, add);
+  cnt = wave_reduce(cnt, [](int p, int q) { return p + q; });
+  const auto imin = [](int p, int q) { return min(p, q); };
+  if (DRAFT) {
+    wave_min2(f1, f2);
+    g = wave_reduce(g, imin);
+  } else {
+    f1 = wave_reduce(f1, imin);
+  }
+  if (lane == 0) {
+    red.zs[0][wave] = zz;
+    red.zs[1][wave] = ss;
+    red.cnt[wave] = cnt;
+    red.idx[0][wave] = f1;
+    red.idx[1][wave] = f2;
+    red.idx[2][wave] = g;
+  }
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  zz = (red.zs[0][0] + red.zs[0][1]) + (red.zs[0][2] + red.zs[0][3]);
+  ss = (red.zs[1][0] + red.zs[1][1]) + (red.zs[1][2] + red.zs[1][3]);
+  cnt = red.cnt[0] + red.cnt[1] + red.cnt[2] + red.cnt[3];
+  f1 = red.idx[0][0];
+  f2 = red.idx[1][0];
+  g = red.idx[2][0];
+  for (int w = 1; w < kLogitThreads / 64; ++w) {
+    if (DRAFT) min2_merge(f1, f2, red.idx[0][w], red.idx[1][w]);
+    else f1 = min(f1, red.idx[0][w]);
+    g = min(g, red.idx[2][w]);
+  }
+  i1 = f1;
+  i2 = !DRAFT ? kNoIndex : (v2 == m ? f2 : g);
+  z = zz + (float)(cnt - 1);
+  s = ss * kLn2;
 }
 
 struct State {
@@ -248,16 +292,27 @@ __device__ __forceinline__ State shfl_state(const State& x, int off) {
                __shfl_xor(x.i2, off), __shfl_xor(x.zp, off), __shfl_xor(x.s, off)};
 }
 
-// One wave merges `count` states: lane k takes states k, k+64, ... in order,
-// then a fixed butterfly combines the lanes.  Every lane ends with the result.
+// Lanes per row when a row's chunk states are merged by a lane group: the
+// smallest power of two >= nchunk, at most 64 (a group never spans waves).
+__device__ __forceinline__ int group_lanes(int nchunk) {
+  int l = 1;
+  while (l < nchunk && l < 64) l <<= 1;
+  return l;
+}
+
+// A group of `lanes` consecutive lanes merges `count` states: lane j of the
+// group takes states j, j + lanes, ... in order, then a fixed butterfly
+// combines the group.  Every lane of the group ends with the result.  All
+// states of all groups are fetched at once, so a pass costs one round trip.
 template <typename Fetch>
-__device__ __forceinline__ State wave_merge(int count, Fetch fetch) {
-  const int lane = threadIdx.x & 63;
+__device__ __forceinline__ State group_merge(int lanes, int count, bool active, Fetch fetch) {
+  const int j = (threadIdx.x & 63) & (lanes - 1);
   State acc{kNegInf, kNoIndex, kNegInf, kNoIndex, 0.f, 0.f};
-  for (int k = lane; k < count; k += 64) acc = merge(acc, fetch(k));
-  for (int off = 1; off < 64; off <<= 1) {
+  if (active)
+    for (int k = j; k < count; k += lanes) acc = merge(acc, fetch(k));
+  for (int off = 1; off < lanes; off <<= 1) {
     const State o = shfl_state(acc, off);
-    acc = (lane & off) ? merge(o, acc) : merge(acc, o);  // same operand order in both partners
+    acc = (j & off) ? merge(o, acc) : merge(acc, o);  // same operand order in both partners
   }
   return acc;
 }
@@ -280,24 +335,30 @@ __global__ __launch_bounds__(kLogitThreads) void verify_rows_kernel(VerifyArgs a
 __global__ __launch_bounds__(kLogitThreads) void verify_finalize_kernel(VerifyArgs a) {
   __shared__ int s_am[kBatchRows];
   __shared__ float s_h[kBatchRows];
+  __shared__ int s_tok[kBatchRows];
   const int r = blockIdx.x;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int k0 = a.row_indptr[r], k1 = a.row_indptr[r + 1];
   const int nrows = k1 - k0;
+  const int lanes = group_lanes(a.nchunk);
+  const int per_pass = kLogitThreads / lanes;  // rows merged per pass
   int acc_len = nrows;  // kept by wave 0
   int next = -1;
   bool found = false;
   float hsum = 0.f;
   for (int b0 = 0; b0 < nrows; b0 += kBatchRows) {
     const int nb = min(kBatchRows, nrows - b0);
-    for (int i = wave; i < nb; i += kLogitThreads / 64) {
-      const int row = k0 + b0 + i;
-      const float4* cs = a.chunk_st + (size_t)row * a.nchunk;
-      const State st = wave_merge(a.nchunk, [&](int k) {
+    for (int j = tid; j < nb; j += kLogitThreads) s_tok[j] = a.tokens[k0 + b0 + j];
+    for (int i0 = 0; i0 < nb; i0 += per_pass) {
+      const int i = i0 + tid / lanes;
+      const bool active = i < nb;
+      const float4* cs = a.chunk_st + (size_t)(k0 + b0 + (active ? i : 0)) * a.nchunk;
+      const State st = group_merge(lanes, a.nchunk, active, [&](int k) {
         const float4 q = cs[k];
         return State{q.x, __float_as_int(q.y), kNegInf, kNoIndex, q.z, q.w};
       });
-      if (lane == 0) {
+      if (active && (tid & (lanes - 1)) == 0) {
+        const int row = k0 + b0 + i;
         const float h = entropy_of(st);
         a.row_argmax[row] = st.i1;
         if (a.row_entropy) a.row_entropy[row] = h;
@@ -313,7 +374,7 @@ __global__ __launch_bounds__(kLogitThreads) void verify_finalize_kernel(VerifyAr
         bool mis = false;
         float h = 0.f;
         if (j < nb) {
-          const int tok = a.tokens[k0 + b0 + j];
+          const int tok = s_tok[j];
           mis = tok < 0 || s_am[j] != tok;
           h = s_h[j];
         }
@@ -356,16 +417,16 @@ __global__ __launch_bounds__(kLogitThreads) void draft_rows_kernel(DraftArgs a) 
 }
 
 __global__ __launch_bounds__(kLogitThreads) void draft_finalize_kernel(DraftArgs a) {
-  const int row = blockIdx.x * (kLogitThreads / 64) + (threadIdx.x >> 6);
-  if (row >= a.rows) return;
-  const float4* ca = a.chunk_a + (size_t)row * a.nchunk;
-  const float2* cb = a.chunk_b + (size_t)row * a.nchunk;
-  const State st = wave_merge(a.nchunk, [&](int k) {
-    const float4 q = ca[k];
-    const float2 w = cb[k];
+  const int lanes = group_lanes(a.nchunk);
+  const int row = blockIdx.x * (kLogitThreads / lanes) + (int)threadIdx.x / lanes;
+  const bool active = row < a.rows;
+  const size_t base = (size_t)(active ? row : 0) * a.nchunk;
+  const State st = group_merge(lanes, a.nchunk, active, [&](int k) {
+    const float4 q = a.chunk_a[base + k];
+    const float2 w = a.chunk_b[base + k];
     return State{q.x, __float_as_int(q.y), q.z, __float_as_int(q.w), w.x, w.y};
   });
-  if ((threadIdx.x & 63) == 0) {
+  if (active && (threadIdx.x & (lanes - 1)) == 0) {
     const float zinv = 1.f / (1.f + st.zp);
     const float d2 = st.v2 - st.m;  // <= 0
     a.top1[row] = st.i1;
@@ -394,7 +455,11 @@ hipError_t launch_draft(const DraftArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(draft_rows_kernel, dim3(a.grid_rows), dim3(kLogitThreads), 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(draft_finalize_kernel, dim3((a.rows + 3) / 4), dim3(kLogitThreads), 0, stream, a);
+  int lanes = 1;
+  while (lanes < a.nchunk && lanes < 64) lanes <<= 1;
+  const int rows_per_group = kLogitThreads / lanes;
+  hipLaunchKernelGGL(draft_finalize_kernel, dim3((a.rows + rows_per_group - 1) / rows_per_group), dim3(kLogitThreads),
+                     0, stream, a);
   return hipGetLastError();
 }
 
