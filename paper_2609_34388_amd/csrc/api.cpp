@@ -220,6 +220,7 @@ rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t
   a.g = layout->num_q_heads / layout->num_kv_heads;
   a.sm_scale = layout->sm_scale > 0.f ? layout->sm_scale : 1.0f / std::sqrt((float)layout->head_dim);
   a.scale_log2 = a.sm_scale * 1.4426950408889634f;
+  a.rescale_gap = 8.0f / a.scale_log2;
   hipStream_t s = static_cast<hipStream_t>(stream);
   for (const AttnPlan& p : fp.launches) {
     if (p.total_items == 0) continue;

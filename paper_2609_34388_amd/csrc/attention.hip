@@ -9,28 +9,30 @@
 //
 // Work decomposition.  A work item is (request, KV head, column group, KV
 // chunk).  Its "columns" are all (query token, query head) pairs of the
-// request that share the KV head -- n * Hq/Hkv of them -- so every K/V byte
-// of a chunk is read from HBM once for all of them.  Each of the 4 waves owns
-// one or two 32-column tiles.  Requests whose keys span several chunks write
-// un-normalised partial outputs plus (max, sum) per column; a second kernel
-// merges them with the usual log-sum-exp weights.
+// request that share the KV head -- n * Hq/Hkv of them, up to 256 per group --
+// so every K/V byte of a chunk is read from HBM once for all of them.  The 8
+// waves of a work group split the group into 32-column tiles and, when there
+// are fewer than 8 tiles, the chunk's 32-key sub-tiles into key groups.
+// Requests whose keys span several chunks write un-normalised partial outputs
+// plus (max, sum) per column; a second kernel merges them with the usual
+// log-sum-exp weights.
 //
-// Per 64-key step the work group stages K and V of four 16-token pages into
-// LDS (double buffered; the next step's global loads are in flight while the
-// current step computes).  On each 32-key sub-tile a wave forms
-// S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (K rows are the MFMA rows, query
-// columns the MFMA columns), applies the mask, updates the running max and
-// sum in fp32 (exp2 with the scale folded in), converts P to bf16 and
-// accumulates O^T += V^T P^T with the same MFMA.  The K rows of a sub-tile
-// are loaded in a permuted order (bits 2 and 3 of the row index swapped) so
-// that the S^T accumulator registers a lane holds are exactly the P^T operand
-// the PV MFMA needs and the matching V^T operand is 8 consecutive keys of one
-// head dimension: 16 contiguous bytes of a dimension-major V page.
+// K and V of 128 keys (8 pages) at a time are copied straight into LDS
+// (double buffered: the next buffer's copies are in flight while the current
+// one is computed).  On each 32-key sub-tile a wave forms S^T = K Q^T with
+// v_mfma_f32_32x32x16_bf16 (K rows are the MFMA rows, query columns the MFMA
+// columns), applies the mask, updates the running max and sum in fp32 (exp2
+// with the scale folded in), converts P to bf16 and accumulates
+// O^T += V^T P^T with the same MFMA.  The K rows of a sub-tile are loaded in a
+// permuted order (bits 2 and 3 of the row index swapped) so that the S^T
+// accumulator registers a lane holds are exactly the P^T operand the PV MFMA
+// needs and the matching V^T operand is 8 consecutive keys of one head
+// dimension: 16 contiguous bytes of a dimension-major V page.
 //
 // Bounds: a work group loads only keys of its own chunk, which ends at or
-// before T, so unused slots of a request's last page are never read; staged
-// K rows and V entries past the chunk end are zero-filled and their scores
-// masked to -inf.
+// before T, so unused slots of a request's last page are never read; buffer
+// rows past the chunk end are filled from the chunk's last key, their scores
+// masked to -inf and their values zeroed.
 #include "rg_internal.h"
 
 namespace rg {
@@ -303,9 +305,12 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
       const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
       mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
     }
-    const float m_new = fmaxf(m_run, mx);
-    const bool grew = m_new > m_run;
+    // The reference maximum only moves when a score exceeds it by more than
+    // 2^8 in probability: P stays below 256 (exact enough in bf16, far from
+    // overflow in fp32) and the accumulator is rescaled rarely.
+    const bool grew = mx > m_run + a.rescale_gap;
     if (__any(grew)) {
+      const float m_new = grew ? mx : m_run;
       const float alpha = grew ? __builtin_amdgcn_exp2f((m_run - m_new) * a.scale_log2) : 1.f;
       l_run *= alpha;
 #pragma unroll
@@ -314,7 +319,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
         for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
       m_run = m_new;
     }
-    const float mc = (m_new == kNegInf) ? 0.f : m_new * a.scale_log2;
+    const float mc = (m_run == kNegInf) ? 0.f : m_run * a.scale_log2;
     u32x4 pk[2];
 #pragma unroll
     for (int pp = 0; pp < 2; ++pp)

@@ -52,7 +52,8 @@ struct AttnArgs {
   float* part_ml;  // [partial columns][2] fp32 (running max of raw scores, sum)
   int32_t hq, hkv, g;
   float sm_scale;    // natural-log domain scale
-  float scale_log2;  // sm_scale * log2(e)
+  float scale_log2;   // sm_scale * log2(e)
+  float rescale_gap;  // raw-score margin before the running maximum moves
 };
 
 // Attention launchers (attention.hip).  `plan` is one launch's plan.
