@@ -113,8 +113,9 @@ rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
       const int64_t ncg = (M + fp.cols_per_group - 1) / fp.cols_per_group;
       items += hkv * ncg * nch;
       if (nch > 1) {
-        part += hkv * nch * M;
-        comb += hkv * ((M + 3) / 4);
+        // partials are stored per 32-column tile, so columns round up to 32
+        part += hkv * nch * round_up(M, 32);
+        comb += hkv * ((M + 31) / 32) * (L->head_dim / 16);  // 128-thread slices of a tile
         fp.split_requests += 1;
       }
       if (items > INT32_MAX / 2 || part > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;

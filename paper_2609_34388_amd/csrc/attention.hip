@@ -367,6 +367,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   }
 
   // Merge the key groups' partial states (lane-wise: same columns, same dims).
+  // A wave's slot holds its accumulator as 16-byte rows, lane-interleaved.
   float l_tot = l_run + __shfl_xor(l_run, 32);
   if (kg > 1) {
     lds_barrier();  // every wave is done with the buffers before they are reused
@@ -375,7 +376,9 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
     if (tile_on && kgi > 0) {
       float* slot = area + (wave - nct2) * PER;
       for (int dt = 0; dt < DT; ++dt)
-        for (int i = 0; i < 16; ++i) slot[(dt * 16 + i) * 64 + lane] = acc[dt][i];
+        for (int ib = 0; ib < 4; ++ib)
+          *(float4*)(slot + ((dt * 4 + ib) * 64 + lane) * 4) =
+              make_float4(acc[dt][4 * ib], acc[dt][4 * ib + 1], acc[dt][4 * ib + 2], acc[dt][4 * ib + 3]);
       slot[64 * 16 * DT + lane] = m_run;
       slot[64 * 16 * DT + 64 + lane] = l_tot;
     }
@@ -390,7 +393,13 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
       const float a0 = __builtin_amdgcn_exp2f((m_run - m_new) * a.scale_log2);
       const float a1 = __builtin_amdgcn_exp2f((mk - m_new) * a.scale_log2);
       for (int dt = 0; dt < DT; ++dt)
-        for (int i = 0; i < 16; ++i) acc[dt][i] = acc[dt][i] * a0 + slot[(dt * 16 + i) * 64 + lane] * a1;
+        for (int ib = 0; ib < 4; ++ib) {
+          const float4 o = *(const float4*)(slot + ((dt * 4 + ib) * 64 + lane) * 4);
+          acc[dt][4 * ib] = acc[dt][4 * ib] * a0 + o.x * a1;
+          acc[dt][4 * ib + 1] = acc[dt][4 * ib + 1] * a0 + o.y * a1;
+          acc[dt][4 * ib + 2] = acc[dt][4 * ib + 2] * a0 + o.z * a1;
+          acc[dt][4 * ib + 3] = acc[dt][4 * ib + 3] * a0 + o.w * a1;
+        }
       l_tot = l_tot * a0 + lk * a1;
       m_run = m_new;
     }
@@ -413,62 +422,89 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
       }
     if (a.lse != nullptr && lh == 0) a.lse[orow] = m_run * a.sm_scale + __logf(l_tot);
   } else {
-    const size_t pcol = (size_t)rq.part_start + ((size_t)hk * nch + c) * M + col;
-    float* dst = a.part_o + pcol * D;
+    // Partial of this 32-column tile, stored in the accumulator's own order:
+    // 16-byte row (dt, ib) of lane l at ((dt * 4 + ib) * 64 + l) * 16 bytes,
+    // so every store instruction writes 1 KiB contiguously.
+    const int M32 = (M + 31) & ~31;
+    const size_t tile0 = (size_t)rq.part_start + ((size_t)hk * nch + c) * M32 + (size_t)(cg * COLS + ct * 32);
+    float* dst = a.part_o + tile0 * D;
     for (int dt = 0; dt < DT; ++dt)
-      for (int ib = 0; ib < 4; ++ib) {
-        const float4 w = make_float4(acc[dt][4 * ib + 0], acc[dt][4 * ib + 1], acc[dt][4 * ib + 2], acc[dt][4 * ib + 3]);
-        *(float4*)(dst + 32 * dt + 8 * ib + 4 * lh) = w;
-      }
-    if (lh == 0) *(float2*)(a.part_ml + 2 * pcol) = make_float2(m_run, l_tot);
+      for (int ib = 0; ib < 4; ++ib)
+        *(float4*)(dst + ((dt * 4 + ib) * 64 + lane) * 4) =
+            make_float4(acc[dt][4 * ib + 0], acc[dt][4 * ib + 1], acc[dt][4 * ib + 2], acc[dt][4 * ib + 3]);
+    if (lh == 0) *(float2*)(a.part_ml + 2 * (tile0 + lc)) = make_float2(m_run, l_tot);
   }
 }
 
-// Merge of the split-KV partials: 4 columns per work group, 64 threads per
-// column, D/64 head dims per thread.
+// Merge of the split-KV partials.  Work item = (request, KV head, 32-column
+// tile, slice of 128 16-byte rows of the tile's fragment-ordered block); a
+// thread owns one row (4 head dims of one column), reads that row and its
+// column's (max, sum) from every chunk -- four chunks' loads in flight at a
+// time -- merges them with online rescaling and writes 4 bf16 outputs.
+constexpr int kCombThreads = 128;
+
 template <int D>
-__global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a, AttnPlan p) {
-  constexpr int PER = D / 64;
+__global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnArgs a, AttnPlan p) {
+  constexpr int SLICES = 8 * D / kCombThreads;  // 16-byte rows per tile block / threads
   const int item = xcd_item(p.grid_comb);
   if (item >= p.total_comb) return;
   const int r = find_request(p, item, true);
   const AttnReq rq = p.req[r];
   const int n = rq.nv & 0xffff, L = rq.ctx, T = L + n;
   const int g = a.g;
-  const int M = n * g;
+  const int M = n * g, M32 = (M + 31) & ~31;
   const int nch = (T + p.chunk - 1) / p.chunk;
-  const int groups = (M + 3) / 4;
-  const int local = item - rq.comb_start;
-  const int hk = local / groups;
-  const int col = (local % groups) * 4 + (threadIdx.x >> 6);
-  if (col >= M) return;
-  const int t = threadIdx.x & 63;
-  const size_t base = (size_t)rq.part_start + (size_t)hk * nch * M + col;
+  int local = item - rq.comb_start;
+  const int slice = local % SLICES;
+  local /= SLICES;
+  const int tiles = M32 / 32;
+  const int tile = local % tiles;
+  const int hk = local / tiles;
+  const int f = slice * kCombThreads + (int)threadIdx.x;  // row of the block
+  const int lane = f & 63, lc = lane & 31, lh = lane >> 5, q = f >> 6;
+  const size_t base = (size_t)rq.part_start + (size_t)hk * nch * M32 + (size_t)tile * 32;
 
-  float mmax = kNegInf;
-  for (int s = 0; s < nch; ++s) mmax = fmaxf(mmax, a.part_ml[2 * (base + (size_t)s * M)]);
-  float lsum = 0.f;
-  float o[PER];
-  for (int e = 0; e < PER; ++e) o[e] = 0.f;
-  for (int s = 0; s < nch; ++s) {
-    const size_t pc = base + (size_t)s * M;
-    const float2 ml = *(const float2*)(a.part_ml + 2 * pc);
-    const float w = __builtin_amdgcn_exp2f((ml.x - mmax) * a.scale_log2);
-    lsum += w * ml.y;
-    const float* src = a.part_o + pc * D + t * PER;
-    for (int e = 0; e < PER; ++e) o[e] += w * src[e];
+  float m = kNegInf, l = 0.f;
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int c0 = 0; c0 < nch; c0 += 4) {
+    float2 ml[4];
+    float4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      ml[u] = make_float2(kNegInf, 0.f);
+      v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (c0 + u < nch) {
+        const size_t t0 = base + (size_t)(c0 + u) * M32;
+        ml[u] = *(const float2*)(a.part_ml + 2 * (t0 + lc));
+        v[u] = *(const float4*)(a.part_o + t0 * D + (size_t)f * 4);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (ml[u].x == kNegInf) continue;  // no key of that chunk is visible to this column
+      const float m_new = fmaxf(m, ml[u].x);
+      const float a0 = __builtin_amdgcn_exp2f((m - m_new) * a.scale_log2);
+      const float a1 = __builtin_amdgcn_exp2f((ml[u].x - m_new) * a.scale_log2);
+      l = l * a0 + ml[u].y * a1;
+      o.x = o.x * a0 + v[u].x * a1;
+      o.y = o.y * a0 + v[u].y * a1;
+      o.z = o.z * a0 + v[u].z * a1;
+      o.w = o.w * a0 + v[u].w * a1;
+      m = m_new;
+    }
   }
-  const int tok = col / g;
-  const int hh = col - tok * g;
+  const int gc = tile * 32 + lc;
+  if (gc >= M) return;
+  const int tok = gc / g;
+  const int hh = gc - tok * g;
   const size_t orow = (size_t)(rq.q_start + tok) * a.hq + hk * g + hh;
-  const float inv = 1.f / lsum;
-  if (PER == 2) {
-    *(uint32_t*)(a.out + orow * D + 2 * t) = pack_bf16x2(o[0] * inv, o[1] * inv);
-  } else {
-    __bf16 b = (__bf16)(o[0] * inv);
-    a.out[orow * D + t] = __builtin_bit_cast(uint16_t, b);
-  }
-  if (a.lse != nullptr && t == 0) a.lse[orow] = mmax * a.sm_scale + __logf(lsum);
+  const float inv = 1.f / l;
+  const int d0 = 32 * (q >> 2) + 8 * (q & 3) + 4 * lh;
+  u32x2 w;
+  w[0] = pack_bf16x2(o.x * inv, o.y * inv);
+  w[1] = pack_bf16x2(o.z * inv, o.w * inv);
+  *(u32x2*)(a.out + orow * D + d0) = w;
+  if (a.lse != nullptr && f < 32) a.lse[orow] = m * a.sm_scale + __logf(l);
 }
 
 template <int D>
@@ -477,7 +513,7 @@ hipError_t launch_impl(const AttnArgs& args, const AttnPlan& plan, hipStream_t s
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (plan.total_comb > 0) {
-    hipLaunchKernelGGL((attn_combine_kernel<D>), dim3(plan.grid_comb), dim3(256), 0, stream, args, plan);
+    hipLaunchKernelGGL((attn_combine_kernel<D>), dim3(plan.grid_comb), dim3(kCombThreads), 0, stream, args, plan);
     e = hipGetLastError();
   }
   return e;

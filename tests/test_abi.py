@@ -134,7 +134,7 @@ def test_plan_accounting(name):
         items += s.num_kv_heads * (-(-M // cpg)) * nch
         if nch > 1:
             split += 1
-            part += s.num_kv_heads * nch * M
+            part += s.num_kv_heads * nch * (-(-M // 32) * 32)  # partials per 32-column tile
     assert info.work_items == items
     assert info.split_requests == split
     assert info.partial_columns == part
