@@ -11,8 +11,9 @@
 // chunk).  Its "columns" are all (query token, query head) pairs of the
 // request that share the KV head -- n * Hq/Hkv of them, up to 256 per group --
 // so every K/V byte of a chunk is read from HBM once for all of them.  The 8
-// waves of a work group split the group into 32-column tiles and, when there
-// are fewer than 8 tiles, the chunk's 32-key sub-tiles into key groups.
+// compute waves of a work group split the group into 32-column tiles and,
+// when there are fewer than 8 tiles, the chunk's 32-key sub-tiles into key
+// groups; 4 more waves only issue the copies into LDS.
 // Requests whose keys span several chunks write un-normalised partial outputs
 // plus (max, sum) per column; a second kernel merges them with the usual
 // log-sum-exp weights.
@@ -29,10 +30,10 @@
 // needs and the matching V^T operand is 8 consecutive keys of one head
 // dimension: 16 contiguous bytes of a dimension-major V page.
 //
-// Bounds: a work group loads only keys of its own chunk, which ends at or
-// before T, so unused slots of a request's last page are never read; buffer
-// rows past the chunk end are filled from the chunk's last key, their scores
-// masked to -inf and their values zeroed.
+// Bounds: a work group reads only pages of its own chunk (whole pages of the
+// pool, unused slots of a request's last page included); buffer rows past
+// the chunk end get their scores masked to -inf and their values zeroed, so
+// whatever those slots hold (NaN included) never reaches the output.
 #include "rg_internal.h"
 
 namespace rg {
@@ -124,8 +125,9 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-constexpr int kWaves = 8;    // waves per work group (two per SIMD)
-constexpr int kThreads = 64 * kWaves;
+constexpr int kWaves = 8;      // compute waves per work group (two per SIMD)
+constexpr int kProducers = 4;  // copy waves per work group (one per SIMD)
+constexpr int kThreads = 64 * (kWaves + kProducers);
 constexpr int kSuper = 128;  // keys staged per LDS buffer (four 32-key sub-tiles)
 constexpr int kBufs = 2;     // LDS buffers: one computed, one being filled
 static_assert(kSuper % kKeyTile == 0, "a super-tile is a whole number of key tiles");
@@ -140,8 +142,10 @@ static_assert(kSuper % kKeyTile == 0, "a super-tile is a whole number of key til
 //
 // Keys stream through two LDS buffers of 128 keys (K and V of 8 pages).
 // While one buffer is computed the next one is filled by LDS-DMA; there is
-// one barrier per 128 keys, so the two waves sharing a SIMD drift out of
-// phase over their sub-tiles and one's MFMAs overlap the other's softmax.
+// one barrier per 128 keys.  The copies are issued by 4 dedicated waves (one
+// per SIMD): a CU accepts a 1 KiB LDS-DMA instruction only every few dozen
+// cycles, and a compute wave issuing its share would stall for most of a
+// buffer's worth of them instead of computing.
 template <int D>
 __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan p) {
   constexpr int NCH = D / 8;                   // 16-byte chunks per K row
@@ -151,10 +155,10 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   constexpr int BLOCKS = SUPER * 2 / 1024;     // 1 KiB DMA blocks per K (or V) buffer
   constexpr int KPB = 1024 / (2 * D);          // keys per K block
   constexpr int VBPP = D / 32;                 // V blocks per page
-  constexpr int G = 2 * BLOCKS / kWaves;       // DMA instructions per wave per buffer
+  constexpr int GP = 2 * BLOCKS / kProducers;  // DMA instructions per copy wave per buffer
   constexpr int MAXPAGES = kMaxChunkKeys / kPageSize;
   constexpr int COLS = 32 * kWaves;            // columns per column group
-  static_assert(2 * BLOCKS % kWaves == 0, "DMA blocks must split evenly over waves");
+  static_assert(2 * BLOCKS % kProducers == 0 && BLOCKS == kProducers * (GP / 2), "DMA blocks split evenly");
   static_assert(kBufs * SUPER * 2 * 2 >= (kWaves - 1) * (64 * 16 * DT + 128) * 4, "merge area");
 
   // buf[b][0] = K of 128 keys ([key][D], 16-byte chunks swizzled per row),
@@ -187,8 +191,9 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   const int nct = min(kWaves, (M - cg * COLS + 31) / 32);
   const int nct2 = nct <= 1 ? 1 : nct <= 2 ? 2 : nct <= 4 ? 4 : 8;
   const int kg = kWaves / nct2;
+  const bool producer = wave >= kWaves;  // wave-uniform: copy wave
   const int ct = wave % nct2, kgi = wave / nct2;
-  const bool tile_on = ct < nct;  // wave-uniform
+  const bool tile_on = !producer && ct < nct;  // wave-uniform
   const int col = cg * COLS + ct * 32 + lc;
   const bool valid = tile_on && col < M;
   const int tok = valid ? col / g : 0;
@@ -217,42 +222,38 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   const char* vbase_g = reinterpret_cast<const char*>(a.v_cache + (size_t)hk * head_stride);
   const size_t page_bytes = (size_t)a.hkv * head_stride * 2;
 
-  // This wave's DMA blocks are b = wave + 8 i.  K blocks hold KPB keys each
-  // and b % 8 = wave fixes both the keys' slots within a page and their
-  // 32-key swizzle, so every K block of the wave uses the same per-lane byte
-  // offset; likewise every V block covers the same head dims (d depends on
-  // b % VBPP only).  Only the page changes from block to block.
-  static_assert((kWaves * KPB) % 32 == 0 && kWaves % VBPP == 0 && BLOCKS % VBPP == 0,
-                "per-wave DMA offsets must not depend on the block");
-  const int kk0 = wave * KPB + lane / NCH;  // key of the lane in block b, minus KPB * 8 i
-  const uint32_t off_k = (uint32_t)((((kk0 % kPageSize) * D) + (((lane % NCH) ^ (swap23(kk0 & 31) & (NCH - 1))) * 8)) * 2);
-  const int dv = (wave % VBPP) * 32 + (lane >> 1);
-  const uint32_t off_v = (uint32_t)((dv * kPageSize + ((lane & 1) ^ vswz(dv)) * 8) * 2);
-
-  // DMA of super-tile s (keys kbeg + 128 s ...) into buffer s % 2.  Keys
-  // past the chunk end read the chunk's last key (a valid token); their
+  // Copy wave pw issues blocks b = pw + 4 i of each buffer: the first GP / 2
+  // are K blocks (KPB keys each), the rest V blocks (32 head dims of a page).
+  // It first reads the page numbers of all its blocks (uniform LDS reads, one
+  // wait), then issues the transfers.  Page slots past the chunk's last page
+  // repeat that page, so buffer rows past the chunk end hold other tokens or
+  // unused slots of the last page (memory of the pool either way); their
   // scores are masked and their values zeroed before use.
+  const int pw = wave - kWaves;
   auto issue = [&](int s) {
-    const int k0 = kbeg + s * kSuper;
-    const bool clamp = k0 + kSuper > kend;  // wave-uniform
+    const int base = s * (kSuper / kPageSize);
+    int pg[GP];
 #pragma unroll
-    for (int i = 0; i < G; ++i) {
-      const int b = wave + i * kWaves;  // wave-uniform
-      const bool is_k = b < BLOCKS;
-      const int slot = is_k ? (b * KPB) / kPageSize : (b - BLOCKS) / VBPP;
-      int page;
-      uint32_t off = is_k ? off_k : off_v;
-      if (!clamp) {
-        page = lds_pages[s * (kSuper / kPageSize) + slot];
+    for (int i = 0; i < GP; ++i) {
+      const int b = pw + i * kProducers;  // wave-uniform
+      const int slot = i < GP / 2 ? (b * KPB) / kPageSize : (b - BLOCKS) / VBPP;
+      pg[i] = lds_pages[min(base + slot, npg - 1)];
+    }
+#pragma unroll
+    for (int i = 0; i < GP; ++i) {
+      const int b = pw + i * kProducers;
+      uint32_t off, dst;
+      if (i < GP / 2) {
+        const int kk = b * KPB + lane / NCH;
+        off = (uint32_t)((((kk % kPageSize) * D) + (((lane % NCH) ^ (swap23(kk & 31) & (NCH - 1))) * 8)) * 2);
+        dst = (uint32_t)(uintptr_t)&buf[s & 1][0][b * 512];
       } else {
-        const int kk = is_k ? b * KPB + lane / NCH : slot * kPageSize;
-        const int key = min(k0 + kk, kend - 1);  // same page for the whole block
-        page = __builtin_amdgcn_readfirstlane(lds_pages[(key >> 4) - pg0]);
-        if (is_k) off += (uint32_t)(((key & (kPageSize - 1)) - (kk & (kPageSize - 1))) * D * 2);
+        const int d = ((b - BLOCKS) % VBPP) * 32 + (lane >> 1);
+        off = (uint32_t)((d * kPageSize + ((lane & 1) ^ vswz(d)) * 8) * 2);
+        dst = (uint32_t)(uintptr_t)&buf[s & 1][1][(b - BLOCKS) * 512];
       }
-      const uint32_t dst = is_k ? (uint32_t)(uintptr_t)&buf[s & 1][0][b * 512]
-                                : (uint32_t)(uintptr_t)&buf[s & 1][1][(b - BLOCKS) * 512];
-      dma16_s((is_k ? kbase_g : vbase_g) + (size_t)__builtin_amdgcn_readfirstlane(page) * page_bytes, off, dst);
+      dma16_s((i < GP / 2 ? kbase_g : vbase_g) + (size_t)__builtin_amdgcn_readfirstlane(pg[i]) * page_bytes, off,
+              dst);
     }
   };
 
@@ -262,16 +263,17 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   float m_run = kNegInf, l_run = 0.f;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  uint32_t koff[KSTEPS];  // byte offsets of this lane's K fragments inside a 32-key sub-tile
-#pragma unroll
-  for (int ks = 0; ks < KSTEPS; ++ks) koff[ks] = (uint32_t)((swap23(lc) * D + (((2 * ks + lh) ^ (lc & (NCH - 1))) * 8)) * 2);
+  // Byte offset of this lane's K fragment ks inside a 32-key sub-tile: row
+  // swap23(lc), 16-byte chunk (2 ks + lh) ^ (lc % NCH) = 2 (ks ^ kw) + kb.
+  const int kx = lc & (NCH - 1), kw = kx >> 1;
+  const uint32_t krow = (uint32_t)(swap23(lc) * D * 2 + ((lh ^ (kx & 1)) * 16));
 
   // S^T of sub-tile q (keys 32 q .. 32 q + 31 of the buffer).
   auto qk = [&](const uint16_t* kt, int q) {
     const char* kb = reinterpret_cast<const char*>(kt + 32 * q * D);
     bf16x8 kf[KSTEPS];
 #pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) kf[ks] = *(const bf16x8*)(kb + koff[ks]);
+    for (int ks = 0; ks < KSTEPS; ++ks) kf[ks] = *(const bf16x8*)(kb + krow + ((ks ^ kw) << 5));
     f32x16 sc;
     for (int i = 0; i < 16; ++i) sc[i] = 0.f;
 #pragma unroll
@@ -290,14 +292,6 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
         if (key >= lim) sc[i] = kNegInf;
       }
     }
-    bf16x8 vf[2][DT];
-#pragma unroll
-    for (int pp = 0; pp < 2; ++pp)
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int d = 32 * dt + lc;
-        vf[pp][dt] = *(const bf16x8*)(vt + (2 * q + pp) * (D * kPageSize) + d * kPageSize + ((lh ^ vswz(d)) * 8));
-      }
     float mx = sc[0];
 #pragma unroll
     for (int i = 1; i < 16; ++i) mx = fmaxf(mx, sc[i]);
@@ -332,39 +326,58 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
         pk[pp][e] = __builtin_bit_cast(uint32_t, pb);
       }
 #pragma unroll
-    for (int pp = 0; pp < 2; ++pp)
+    for (int pp = 0; pp < 2; ++pp) {
+      bf16x8 vf[DT];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int d = 32 * dt + lc;
+        vf[dt] = *(const bf16x8*)(vt + (2 * q + pp) * (D * kPageSize) + d * kPageSize + ((lh ^ vswz(d)) * 8));
+      }
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
-        acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[pp][dt], __builtin_bit_cast(bf16x8, pk[pp]), acc[dt], 0, 0, 0);
+        acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[dt], __builtin_bit_cast(bf16x8, pk[pp]), acc[dt], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep the next sub-tile's loads after this one's PV
   };
   const int nsup = (kend - kbeg + kSuper - 1) / kSuper;
-  issue(0);
+  // Plain loads (q) complete before the first LDS-DMA goes out: the compiler
+  // does not count the DMA instructions, and a q load it believed pending
+  // would make it wait for vmcnt(0) -- every copy in flight -- inside the loop.
+  if (producer) issue(0);
   for (int s = 0; s < nsup; ++s) {
-    wait_vmcnt<0>();  // this wave's DMA of super-tile s
-    lds_barrier();    // everyone's: buffer s % 2 is full, buffer (s + 1) % 2 is no longer read
+    if (producer) wait_vmcnt<0>();  // this copy wave's transfers of super-tile s
+    lds_barrier();  // everyone's: buffer s % 2 is full, buffer (s + 1) % 2 is no longer read
     const int k0 = kbeg + s * kSuper;
     const int nvalid = kend - k0;
     const uint16_t* kt = buf[s & 1][0];
     const uint16_t* vt = buf[s & 1][1];
     if (nvalid < kSuper) {
-      // last buffer of the chunk: zero the values of keys past its end
+      // last buffer of the chunk: zero the values of keys past its end, by
+      // 16-byte units (page slot pp, head dim d, half h = keys 16 pp + 8 h ..)
       uint16_t* vz = buf[s & 1][1];
-      for (int i = tid; i < kSuper * D; i += kThreads) {
-        const int kk = i / D, d = i % D;
-        if (kk >= nvalid) {
-          const int pp = kk / kPageSize, kp = kk % kPageSize;
-          vz[pp * (D * kPageSize) + d * kPageSize + (((kp >> 3) ^ vswz(d)) * 8) + (kp & 7)] = 0;
+      for (int u = tid; u < (kSuper / kPageSize) * D * 2; u += kThreads) {
+        const int pp = u / (2 * D), d = (u >> 1) % D, h = u & 1;
+        const int kfirst = kPageSize * pp + 8 * h;
+        if (kfirst + 8 <= nvalid) continue;
+        uint16_t* unit = vz + pp * (D * kPageSize) + d * kPageSize + ((h ^ vswz(d)) * 8);
+        if (kfirst >= nvalid) {
+          *(u32x4*)unit = u32x4{0u, 0u, 0u, 0u};
+        } else {
+          for (int e = nvalid - kfirst; e < 8; ++e) unit[e] = 0;
         }
       }
       lds_barrier();
     }
-    if (s + 1 < nsup) issue(s + 1);
-    if (tile_on) {
+    if (producer) {
+      if (s + 1 < nsup) issue(s + 1);
+    } else if (tile_on) {
       // this wave's sub-tiles of the buffer: global sub-tile j = 4 s + q with j % kg == kgi
       for (int q = 0; q < kSuper / 32; ++q)
         if ((4 * s + q) % kg == kgi && 32 * q < nvalid) softmax_pv(qk(kt, q), k0 + 32 * q, vt, q);
     }
   }
+
+  if (producer) return;
 
   // Merge the key groups' partial states (lane-wise: same columns, same dims).
   // A wave's slot holds its accumulator as 16-byte rows, lane-interleaved.
