@@ -60,14 +60,18 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
+// Request owning work item `item`: the last r with start(r) <= item (starts
+// are nondecreasing, empty requests share their successor's start).  Every
+// lane tests one request, so the search is one round of loads, not a chain.
 __device__ __forceinline__ int find_request(const AttnPlan& p, int item, bool combine) {
-  int lo = 0, hi = p.num_req - 1;
-  while (lo < hi) {
-    int mid = (lo + hi + 1) >> 1;
-    int start = combine ? p.req[mid].comb_start : p.req[mid].item_start;
-    if (start <= item) lo = mid; else hi = mid - 1;
+  const int lane = threadIdx.x & 63;
+  int r = 0;
+  for (int base = 1; base < p.num_req; base += 64) {
+    const int k = base + lane;
+    const bool le = k < p.num_req && (combine ? p.req[k].comb_start : p.req[k].item_start) <= item;
+    r += __popcll(__ballot(le));
   }
-  return lo;
+  return __builtin_amdgcn_readfirstlane(r);
 }
 
 // Consecutive work items of one (request, KV head) land on one XCD: the
@@ -452,7 +456,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
 // Merge of the split-KV partials.  Work item = (request, KV head, 32-column
 // tile, slice of 128 16-byte rows of the tile's fragment-ordered block); a
 // thread owns one row (4 head dims of one column), reads that row and its
-// column's (max, sum) from every chunk -- four chunks' loads in flight at a
+// column's (max, sum) from every chunk -- eight chunks' loads in flight at a
 // time -- merges them with online rescaling and writes 4 bf16 outputs.
 constexpr int kCombThreads = 128;
 
@@ -479,11 +483,11 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnArgs a, 
 
   float m = kNegInf, l = 0.f;
   float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int c0 = 0; c0 < nch; c0 += 4) {
-    float2 ml[4];
-    float4 v[4];
+  for (int c0 = 0; c0 < nch; c0 += 8) {
+    float2 ml[8];
+    float4 v[8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 8; ++u) {
       ml[u] = make_float2(kNegInf, 0.f);
       v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
       if (c0 + u < nch) {
@@ -493,7 +497,7 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnArgs a, 
       }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 8; ++u) {
       if (ml[u].x == kNegInf) continue;  // no key of that chunk is visible to this column
       const float m_new = fmaxf(m, ml[u].x);
       const float a0 = __builtin_amdgcn_exp2f((m - m_new) * a.scale_log2);
