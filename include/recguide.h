@@ -15,6 +15,7 @@
  *   rg_draft_confidence        draft confidence P_1st, top-2 margin
  *                              P_1st - P_2nd and entropy per draft row
  *                              (Sec. 4.1)
+ *   rg_verify_and_confidence   the two logit passes above in one call
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -182,6 +183,29 @@ rg_status rg_draft_confidence(const uint16_t* logits, int64_t row_stride, int32_
                               int32_t total_rows, int32_t* top1, int32_t* top2, float* p1,
                               float* p2, float* margin, float* entropy, void* ws,
                               size_t ws_bytes, void* stream);
+
+/*
+ * Both logit passes of one round (Sec. 3.1: one forward pass of the fused
+ * step yields the verify rows of the previous block and the rows of the next
+ * draft block) in two launches instead of four.  The results are bit for bit
+ * those of rg_verify_accept(verify_logits, verify_stride, vocab,
+ * num_requests, verify_rows, row_indptr, draft_tokens, row_argmax,
+ * accept_len, next_token, row_entropy, accept_entropy, ...) followed by
+ * rg_draft_confidence(draft_logits, draft_stride, vocab, draft_rows, top1,
+ * top2, p1, p2, margin, entropy, ...); arguments, layouts and NULL rules as
+ * there (vocab >= 2).  One DEVICE workspace of at least the queried size,
+ * 256-byte aligned (RG_ERR_WORKSPACE otherwise).
+ */
+rg_status rg_verify_and_confidence_workspace(int32_t num_requests, int32_t verify_rows,
+                                             int32_t draft_rows, int32_t vocab, size_t* bytes);
+rg_status rg_verify_and_confidence(const uint16_t* verify_logits, int64_t verify_stride,
+                                   const uint16_t* draft_logits, int64_t draft_stride, int32_t vocab,
+                                   int32_t num_requests, int32_t verify_rows,
+                                   const int32_t* row_indptr, const int32_t* draft_tokens,
+                                   int32_t* row_argmax, int32_t* accept_len, int32_t* next_token,
+                                   float* row_entropy, float* accept_entropy, int32_t draft_rows,
+                                   int32_t* top1, int32_t* top2, float* p1, float* p2, float* margin,
+                                   float* entropy, void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -51,7 +51,7 @@ class AttnPlanInfo(ctypes.Structure):
 EXPORTS = ("rg_abi_version", "rg_status_string", "rg_draft_verify_attention_workspace",
            "rg_draft_verify_attention", "rg_draft_verify_attention_plan",
            "rg_verify_accept_workspace", "rg_verify_accept", "rg_draft_confidence_workspace",
-           "rg_draft_confidence")
+           "rg_draft_confidence", "rg_verify_and_confidence_workspace", "rg_verify_and_confidence")
 
 _LIB = None
 
@@ -74,6 +74,9 @@ def _lib():
         "rg_verify_accept": (I32, [P, I64, I32, I32, I32, P, P, P, P, P, P, P, P, SZ, P]),
         "rg_draft_confidence_workspace": (I32, [I32, I32, ctypes.POINTER(SZ)]),
         "rg_draft_confidence": (I32, [P, I64, I32, I32, P, P, P, P, P, P, P, SZ, P]),
+        "rg_verify_and_confidence_workspace": (I32, [I32, I32, I32, I32, ctypes.POINTER(SZ)]),
+        "rg_verify_and_confidence": (I32, [P, I64, P, I64, I32, I32, I32, P, P, P, P, P, P, P,
+                                           I32, P, P, P, P, P, P, P, SZ, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -290,3 +293,56 @@ def draft_confidence(logits: torch.Tensor, *, workspace: Optional[torch.Tensor] 
         _ptr(o.get("entropy")), workspace.data_ptr(), workspace.numel(), _stream(stream))
     _check(st, "rg_draft_confidence")
     return o
+
+
+def verify_and_confidence_workspace_bytes(num_requests: int, verify_rows: int, draft_rows: int, vocab: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib().rg_verify_and_confidence_workspace(num_requests, verify_rows, draft_rows, vocab, ctypes.byref(n)),
+           "rg_verify_and_confidence_workspace")
+    return int(n.value)
+
+
+def verify_and_confidence(verify_logits: torch.Tensor, row_indptr: torch.Tensor, draft_tokens: torch.Tensor,
+                          draft_logits: torch.Tensor, *, workspace: Optional[torch.Tensor] = None,
+                          out_verify: Optional[Dict[str, torch.Tensor]] = None,
+                          out_draft: Optional[Dict[str, torch.Tensor]] = None,
+                          stream=None) -> Tuple[Dict[str, torch.Tensor], Dict[str, torch.Tensor]]:
+    """Both logit passes of a round in one call (rg_verify_and_confidence):
+    returns the outputs of verify_accept and of draft_confidence."""
+    for t, name in ((verify_logits, "verify_logits"), (draft_logits, "draft_logits")):
+        if not t.is_cuda or t.dtype != torch.bfloat16 or t.dim() != 2 or t.stride(1) != 1:
+            raise TypeError(f"{name} must be a CUDA bf16 [rows, vocab] tensor with unit column stride")
+    if verify_logits.shape[1] != draft_logits.shape[1]:
+        raise ValueError("verify and draft logits must have the same vocabulary")
+    _dev(row_indptr, "row_indptr", torch.int32)
+    vrows, vocab = verify_logits.shape
+    drows = draft_logits.shape[0]
+    R = row_indptr.shape[0] - 1
+    if vrows:
+        _dev(draft_tokens, "draft_tokens", torch.int32)
+    dev = verify_logits.device
+    ov = dict(out_verify or {})
+    ov.setdefault("row_argmax", torch.empty(vrows, dtype=torch.int32, device=dev))
+    ov.setdefault("accept_len", torch.empty(R, dtype=torch.int32, device=dev))
+    ov.setdefault("next_token", torch.empty(R, dtype=torch.int32, device=dev))
+    ov.setdefault("row_entropy", torch.empty(vrows, dtype=torch.float32, device=dev))
+    ov.setdefault("accept_entropy", torch.empty(R, dtype=torch.float32, device=dev))
+    od = dict(out_draft or {})
+    for k, dt in (("top1", torch.int32), ("top2", torch.int32), ("p1", torch.float32), ("p2", torch.float32),
+                  ("margin", torch.float32), ("entropy", torch.float32)):
+        od.setdefault(k, torch.empty(drows, dtype=dt, device=dev))
+    if workspace is None:
+        workspace = new_workspace(verify_and_confidence_workspace_bytes(R, vrows, drows, vocab), dev)
+    st = _lib().rg_verify_and_confidence(
+        verify_logits.data_ptr() if vrows else None, verify_logits.stride(0) if vrows else vocab,
+        draft_logits.data_ptr() if drows else None, draft_logits.stride(0) if drows else vocab, vocab, R, vrows,
+        row_indptr.data_ptr(), draft_tokens.data_ptr() if vrows else None,
+        ov["row_argmax"].data_ptr() if vrows else None, ov["accept_len"].data_ptr(), ov["next_token"].data_ptr(),
+        _ptr(ov.get("row_entropy")) if vrows else None, _ptr(ov.get("accept_entropy")), drows,
+        _ptr(od["top1"]) if drows else None, _ptr(od["top2"]) if drows else None,
+        _ptr(od["p1"]) if drows else None, _ptr(od["p2"]) if drows else None,
+        _ptr(od.get("margin")) if drows else None, _ptr(od.get("entropy")) if drows else None,
+        workspace.data_ptr(), workspace.numel(), _stream(stream))
+    _check(st, "rg_verify_and_confidence")
+    return ov, od
+

@@ -237,11 +237,14 @@ rg_status rg_verify_accept_workspace(int32_t num_requests, int32_t total_rows, i
   return RG_OK;
 }
 
-rg_status rg_verify_accept(const uint16_t* logits, int64_t row_stride, int32_t vocab,
-                           int32_t num_requests, int32_t total_rows, const int32_t* row_indptr,
-                           const int32_t* draft_tokens, int32_t* row_argmax, int32_t* accept_len,
-                           int32_t* next_token, float* row_entropy, float* accept_entropy,
-                           void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+rg_status make_verify_args(const uint16_t* logits, int64_t row_stride, int32_t vocab, int32_t num_requests,
+                           int32_t total_rows, const int32_t* row_indptr, const int32_t* draft_tokens,
+                           int32_t* row_argmax, int32_t* accept_len, int32_t* next_token, float* row_entropy,
+                           float* accept_entropy, void* ws, size_t ws_bytes, VerifyArgs& a) {
   if (num_requests < 1 || total_rows < 0 || vocab < 1) return RG_ERR_SHAPE;
   if (!row_indptr || !accept_len || !next_token) return RG_ERR_NULL;
   if (total_rows > 0 && (!logits || !draft_tokens || !row_argmax)) return RG_ERR_NULL;
@@ -249,8 +252,6 @@ rg_status rg_verify_accept(const uint16_t* logits, int64_t row_stride, int32_t v
   if ((int64_t)total_rows * logit_chunks(vocab) > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
   const size_t need = verify_ws_bytes(total_rows, vocab);
   if (total_rows > 0 && (ws == nullptr || ws_bytes < need || !aligned(ws, 16))) return RG_ERR_WORKSPACE;
-
-  VerifyArgs a;
   std::memset(&a, 0, sizeof(a));
   a.logits = logits;
   a.row_stride = row_stride;
@@ -268,29 +269,18 @@ rg_status rg_verify_accept(const uint16_t* logits, int64_t row_stride, int32_t v
   a.chunk_st = static_cast<float4*>(ws);
   a.vec = (aligned(logits, 16) && row_stride % 8 == 0) ? 1 : 0;
   a.grid_rows = (int32_t)round_up((int64_t)total_rows * a.nchunk, 8);
-  return launch_verify(a, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
-}
-
-rg_status rg_draft_confidence_workspace(int32_t total_rows, int32_t vocab, size_t* bytes) {
-  if (bytes == nullptr) return RG_ERR_NULL;
-  if (total_rows < 0 || vocab < 2) return RG_ERR_SHAPE;
-  *bytes = draft_ws_bytes(total_rows, vocab);
   return RG_OK;
 }
 
-rg_status rg_draft_confidence(const uint16_t* logits, int64_t row_stride, int32_t vocab,
-                              int32_t total_rows, int32_t* top1, int32_t* top2, float* p1,
-                              float* p2, float* margin, float* entropy, void* ws,
-                              size_t ws_bytes, void* stream) {
+rg_status make_draft_args(const uint16_t* logits, int64_t row_stride, int32_t vocab, int32_t total_rows,
+                          int32_t* top1, int32_t* top2, float* p1, float* p2, float* margin, float* entropy,
+                          void* ws, size_t ws_bytes, DraftArgs& a) {
   if (total_rows < 0 || vocab < 2) return RG_ERR_SHAPE;
   if (total_rows > 0 && (!logits || !top1 || !top2 || !p1 || !p2)) return RG_ERR_NULL;
   if (row_stride < vocab) return RG_ERR_SHAPE;
   if ((int64_t)total_rows * logit_chunks(vocab) > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
   const size_t need = draft_ws_bytes(total_rows, vocab);
   if (total_rows > 0 && (ws == nullptr || ws_bytes < need || !aligned(ws, 16))) return RG_ERR_WORKSPACE;
-  if (total_rows == 0) return RG_OK;
-
-  DraftArgs a;
   std::memset(&a, 0, sizeof(a));
   a.logits = logits;
   a.row_stride = row_stride;
@@ -305,12 +295,80 @@ rg_status rg_draft_confidence(const uint16_t* logits, int64_t row_stride, int32_
   a.entropy = entropy;
   char* w = static_cast<char*>(ws);
   a.chunk_a = reinterpret_cast<float4*>(w);
-  w += align256((size_t)total_rows * a.nchunk * 16);
+  if (w != nullptr) w += align256((size_t)total_rows * a.nchunk * 16);
   a.chunk_b = reinterpret_cast<float2*>(w);
   a.vec = (aligned(logits, 16) && row_stride % 8 == 0) ? 1 : 0;
   a.grid_rows = (int32_t)round_up((int64_t)total_rows * a.nchunk, 8);
+  return RG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rg_status rg_verify_accept(const uint16_t* logits, int64_t row_stride, int32_t vocab,
+                           int32_t num_requests, int32_t total_rows, const int32_t* row_indptr,
+                           const int32_t* draft_tokens, int32_t* row_argmax, int32_t* accept_len,
+                           int32_t* next_token, float* row_entropy, float* accept_entropy,
+                           void* ws, size_t ws_bytes, void* stream) {
+  VerifyArgs a;
+  const rg_status st = make_verify_args(logits, row_stride, vocab, num_requests, total_rows, row_indptr,
+                                        draft_tokens, row_argmax, accept_len, next_token, row_entropy,
+                                        accept_entropy, ws, ws_bytes, a);
+  if (st != RG_OK) return st;
+  return launch_verify(a, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
+
+rg_status rg_draft_confidence_workspace(int32_t total_rows, int32_t vocab, size_t* bytes) {
+  if (bytes == nullptr) return RG_ERR_NULL;
+  if (total_rows < 0 || vocab < 2) return RG_ERR_SHAPE;
+  *bytes = draft_ws_bytes(total_rows, vocab);
+  return RG_OK;
+}
+
+rg_status rg_draft_confidence(const uint16_t* logits, int64_t row_stride, int32_t vocab,
+                              int32_t total_rows, int32_t* top1, int32_t* top2, float* p1,
+                              float* p2, float* margin, float* entropy, void* ws,
+                              size_t ws_bytes, void* stream) {
+  DraftArgs a;
+  const rg_status st = make_draft_args(logits, row_stride, vocab, total_rows, top1, top2, p1, p2, margin,
+                                       entropy, ws, ws_bytes, a);
+  if (st != RG_OK) return st;
+  if (total_rows == 0) return RG_OK;
   return launch_draft(a, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
 }
 
+rg_status rg_verify_and_confidence_workspace(int32_t num_requests, int32_t verify_rows, int32_t draft_rows,
+                                             int32_t vocab, size_t* bytes) {
+  if (bytes == nullptr) return RG_ERR_NULL;
+  if (num_requests < 1 || verify_rows < 0 || draft_rows < 0 || vocab < 2) return RG_ERR_SHAPE;
+  *bytes = align256(verify_ws_bytes(verify_rows, vocab)) + draft_ws_bytes(draft_rows, vocab);
+  return RG_OK;
+}
+
+rg_status rg_verify_and_confidence(const uint16_t* verify_logits, int64_t verify_stride,
+                                   const uint16_t* draft_logits, int64_t draft_stride, int32_t vocab,
+                                   int32_t num_requests, int32_t verify_rows, const int32_t* row_indptr,
+                                   const int32_t* draft_tokens, int32_t* row_argmax, int32_t* accept_len,
+                                   int32_t* next_token, float* row_entropy, float* accept_entropy,
+                                   int32_t draft_rows, int32_t* top1, int32_t* top2, float* p1, float* p2,
+                                   float* margin, float* entropy, void* ws, size_t ws_bytes, void* stream) {
+  if (vocab < 2 || verify_rows < 0 || draft_rows < 0) return RG_ERR_SHAPE;
+  const size_t vbytes = align256(verify_ws_bytes(verify_rows, vocab));
+  const size_t dbytes = draft_ws_bytes(draft_rows, vocab);
+  if (vbytes + dbytes > 0 && (ws == nullptr || ws_bytes < vbytes + dbytes || !aligned(ws, 256)))
+    return RG_ERR_WORKSPACE;
+  char* w = static_cast<char*>(ws);
+  VerifyArgs v;
+  rg_status st = make_verify_args(verify_logits, verify_stride, vocab, num_requests, verify_rows, row_indptr,
+                                  draft_tokens, row_argmax, accept_len, next_token, row_entropy, accept_entropy,
+                                  w, vbytes, v);
+  if (st != RG_OK) return st;
+  DraftArgs d;
+  st = make_draft_args(draft_logits, draft_stride, vocab, draft_rows, top1, top2, p1, p2, margin, entropy,
+                       dbytes ? w + vbytes : nullptr, dbytes, d);
+  if (st != RG_OK) return st;
+  return launch_round(v, d, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
 
 }  // extern "C"

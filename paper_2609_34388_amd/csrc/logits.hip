@@ -320,10 +320,8 @@ __device__ __forceinline__ State group_merge(int lanes, int count, bool active, 
 __device__ __forceinline__ float entropy_of(const State& st) { return log1pf(st.zp) - st.s / (1.f + st.zp); }
 
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kLogitThreads) void verify_rows_kernel(VerifyArgs a) {
-  __shared__ ChunkRed red;
-  const int item = xcd_item(a.grid_rows);
-  if (item >= a.rows * a.nchunk) return;
+// One (row, chunk) item of the verify rows.
+__device__ __forceinline__ void verify_rows(const VerifyArgs& a, int item, ChunkRed& red) {
   const int row = item / a.nchunk, c = item % a.nchunk;
   const int v0 = c * kLogitChunk, v1 = min(a.vocab, v0 + kLogitChunk);
   float m, v2, z, s;
@@ -332,11 +330,24 @@ __global__ __launch_bounds__(kLogitThreads) void verify_rows_kernel(VerifyArgs a
   if (threadIdx.x == 0) a.chunk_st[(size_t)row * a.nchunk + c] = make_float4(m, __int_as_float(i1), z, s);
 }
 
-__global__ __launch_bounds__(kLogitThreads) void verify_finalize_kernel(VerifyArgs a) {
-  __shared__ int s_am[kBatchRows];
-  __shared__ float s_h[kBatchRows];
-  __shared__ int s_tok[kBatchRows];
-  const int r = blockIdx.x;
+__global__ __launch_bounds__(kLogitThreads) void verify_rows_kernel(VerifyArgs a) {
+  __shared__ ChunkRed red;
+  const int item = xcd_item(a.grid_rows);
+  if (item < a.rows * a.nchunk) verify_rows(a, item, red);
+}
+
+struct FinalizeLds {
+  int am[kBatchRows];
+  float h[kBatchRows];
+  int tok[kBatchRows];
+};
+
+// Request r of the verify rows: merge each row's chunk states, then the
+// first mismatch, next token and e_t.
+__device__ __forceinline__ void verify_finalize(const VerifyArgs& a, int r, FinalizeLds& lds) {
+  int* s_am = lds.am;
+  float* s_h = lds.h;
+  int* s_tok = lds.tok;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int k0 = a.row_indptr[r], k1 = a.row_indptr[r + 1];
   const int nrows = k1 - k0;
@@ -399,11 +410,14 @@ __global__ __launch_bounds__(kLogitThreads) void verify_finalize_kernel(VerifyAr
   }
 }
 
+__global__ __launch_bounds__(kLogitThreads) void verify_finalize_kernel(VerifyArgs a) {
+  __shared__ FinalizeLds lds;
+  verify_finalize(a, blockIdx.x, lds);
+}
+
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kLogitThreads) void draft_rows_kernel(DraftArgs a) {
-  __shared__ ChunkRed red;
-  const int item = xcd_item(a.grid_rows);
-  if (item >= a.rows * a.nchunk) return;
+// One (row, chunk) item of the draft rows.
+__device__ __forceinline__ void draft_rows(const DraftArgs& a, int item, ChunkRed& red) {
   const int row = item / a.nchunk, c = item % a.nchunk;
   const int v0 = c * kLogitChunk, v1 = min(a.vocab, v0 + kLogitChunk);
   float m, v2, z, s;
@@ -416,9 +430,16 @@ __global__ __launch_bounds__(kLogitThreads) void draft_rows_kernel(DraftArgs a) 
   }
 }
 
-__global__ __launch_bounds__(kLogitThreads) void draft_finalize_kernel(DraftArgs a) {
+__global__ __launch_bounds__(kLogitThreads) void draft_rows_kernel(DraftArgs a) {
+  __shared__ ChunkRed red;
+  const int item = xcd_item(a.grid_rows);
+  if (item < a.rows * a.nchunk) draft_rows(a, item, red);
+}
+
+// Draft rows blk * (256 / lanes) ...: one lane group per row.
+__device__ __forceinline__ void draft_finalize(const DraftArgs& a, int blk) {
   const int lanes = group_lanes(a.nchunk);
-  const int row = blockIdx.x * (kLogitThreads / lanes) + (int)threadIdx.x / lanes;
+  const int row = blk * (kLogitThreads / lanes) + (int)threadIdx.x / lanes;
   const bool active = row < a.rows;
   const size_t base = (size_t)(active ? row : 0) * a.nchunk;
   const State st = group_merge(lanes, a.nchunk, active, [&](int k) {
@@ -438,6 +459,32 @@ __global__ __launch_bounds__(kLogitThreads) void draft_finalize_kernel(DraftArgs
   }
 }
 
+__global__ __launch_bounds__(kLogitThreads) void draft_finalize_kernel(DraftArgs a) { draft_finalize(a, blockIdx.x); }
+
+// Both passes of one round in two launches: the row items of the verify rows
+// and of the draft rows share one grid, and so do the two finalize steps.
+__global__ __launch_bounds__(kLogitThreads) void round_rows_kernel(VerifyArgs v, DraftArgs d, int32_t grid) {
+  __shared__ ChunkRed red;
+  const int item = xcd_item(grid);
+  const int nv = v.rows * v.nchunk;
+  if (item < nv) verify_rows(v, item, red);
+  else if (item - nv < d.rows * d.nchunk) draft_rows(d, item - nv, red);
+}
+
+__global__ __launch_bounds__(kLogitThreads) void round_finalize_kernel(VerifyArgs v, DraftArgs d) {
+  __shared__ FinalizeLds lds;
+  const int b = blockIdx.x;
+  if (b < v.num_req) verify_finalize(v, b, lds);
+  else draft_finalize(d, b - v.num_req);
+}
+
+int draft_finalize_groups(const DraftArgs& a) {
+  int lanes = 1;
+  while (lanes < a.nchunk && lanes < 64) lanes <<= 1;
+  const int rows_per_group = kLogitThreads / lanes;
+  return (a.rows + rows_per_group - 1) / rows_per_group;
+}
+
 }  // namespace
 
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
@@ -455,11 +502,20 @@ hipError_t launch_draft(const DraftArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(draft_rows_kernel, dim3(a.grid_rows), dim3(kLogitThreads), 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  int lanes = 1;
-  while (lanes < a.nchunk && lanes < 64) lanes <<= 1;
-  const int rows_per_group = kLogitThreads / lanes;
-  hipLaunchKernelGGL(draft_finalize_kernel, dim3((a.rows + rows_per_group - 1) / rows_per_group), dim3(kLogitThreads),
-                     0, stream, a);
+  hipLaunchKernelGGL(draft_finalize_kernel, dim3(draft_finalize_groups(a)), dim3(kLogitThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_round(const VerifyArgs& v, const DraftArgs& d, hipStream_t stream) {
+  const int64_t items = (int64_t)v.rows * v.nchunk + (int64_t)d.rows * d.nchunk;
+  const int32_t grid = (int32_t)((items + 7) / 8 * 8);
+  if (grid > 0) {
+    hipLaunchKernelGGL(round_rows_kernel, dim3(grid), dim3(kLogitThreads), 0, stream, v, d, grid);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int blocks = v.num_req + (d.rows > 0 ? draft_finalize_groups(d) : 0);
+  hipLaunchKernelGGL(round_finalize_kernel, dim3(blocks), dim3(kLogitThreads), 0, stream, v, d);
   return hipGetLastError();
 }
 

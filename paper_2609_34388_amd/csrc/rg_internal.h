@@ -101,5 +101,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream);
 hipError_t launch_draft(const DraftArgs& a, hipStream_t stream);
+// Verify and draft passes of one round together: two launches in all.
+hipError_t launch_round(const VerifyArgs& v, const DraftArgs& d, hipStream_t stream);
 
 }  // namespace rg

@@ -188,3 +188,25 @@ def test_generated_layout_respects_spec_ranges():
     assert lay.page_indices.max() < lay.num_pages
     pages = np.diff(lay.page_indptr)
     assert (pages * 16 >= lay.kv_len).all() and ((pages - 1) * 16 < lay.kv_len).all()
+
+
+def test_fused_round_validation_errors():
+    lib = binding.library()
+    n = ctypes.c_size_t()
+    assert lib.rg_verify_and_confidence_workspace(2, 4, 6, 1, ctypes.byref(n)) == 2  # vocab < 2
+    assert lib.rg_verify_and_confidence_workspace(0, 4, 6, 100, ctypes.byref(n)) == 2
+    assert lib.rg_verify_and_confidence_workspace(2, 4, 6, 20000, None) == 1
+    assert lib.rg_verify_and_confidence_workspace(2, 4, 6, 20000, ctypes.byref(n)) == 0
+    need = n.value
+    sep = ctypes.c_size_t()
+    lib.rg_verify_accept_workspace(2, 4, 20000, ctypes.byref(sep))
+    assert need >= sep.value
+    D = FAKE_DEV
+    def call(ws, ws_bytes, vocab=20000, row_indptr=D, top1=D):
+        return lib.rg_verify_and_confidence(D, vocab, D, vocab, vocab, 2, 4, row_indptr, D, D, D, D, None, None,
+                                            6, top1, D, D, D, None, None, ws, ws_bytes, None)
+    assert call(ctypes.c_void_p(0x10000), need - 1) == 4
+    assert call(ctypes.c_void_p(0x10010), need) == 4  # not 256-byte aligned
+    assert call(ctypes.c_void_p(0x10000), need, row_indptr=None) == 1
+    assert call(ctypes.c_void_p(0x10000), need, top1=None) == 1
+    assert call(ctypes.c_void_p(0x10000), need, vocab=1) == 2

@@ -1,6 +1,6 @@
-"""The three entry points captured in a HIP graph: every replay (with eager
-work and synchronisations in between) must reproduce the eager results bit
-for bit.  The benchmark times such replays."""
+"""The entry points captured in a HIP graph: every replay (with eager work
+and synchronisations in between) must reproduce the eager results bit for
+bit.  The benchmark times such replays."""
 import numpy as np
 import pytest
 import torch
@@ -12,7 +12,8 @@ pytestmark = pytest.mark.gpu
 DEV = torch.device("cuda")
 
 
-def test_graph_replays_match_eager():
+@pytest.mark.parametrize("fused", [False, True])
+def test_graph_replays_match_eager(fused):
     lay = W.make_layout("mid", seed=12, num_requests=6, ctx=("uniform", 300, 2500))
     inp = W.make_attention_inputs(lay, DEV)
     inp.update(W.make_logit_inputs(lay, DEV))
@@ -24,6 +25,8 @@ def test_graph_replays_match_eager():
     vws = binding.new_workspace(binding.verify_accept_workspace_bytes(
         lay.num_requests, lay.total_verify_rows, lay.spec.vocab), DEV)
     dws = binding.new_workspace(binding.draft_confidence_workspace_bytes(lay.total_draft_rows, lay.spec.vocab), DEV)
+    rws = binding.new_workspace(binding.verify_and_confidence_workspace_bytes(
+        lay.num_requests, lay.total_verify_rows, lay.total_draft_rows, lay.spec.vocab), DEV)
     out = torch.empty_like(inp["q"])
     lse = torch.empty(inp["q"].shape[0], lay.spec.num_q_heads, dtype=torch.float32, device=DEV)
     vout = dict(row_argmax=torch.empty(lay.total_verify_rows, dtype=torch.int32, device=DEV),
@@ -38,8 +41,12 @@ def test_graph_replays_match_eager():
     def step():
         binding.draft_verify_attention(inp["q"], inp["k_cache"], inp["v_cache"], None, None, None, None,
                                        page_idx, out=out, lse=lse, workspace=ws, layout=layout)
-        binding.verify_accept(inp["verify_logits"], rp, inp["draft_tokens"], workspace=vws, out=vout)
-        binding.draft_confidence(inp["draft_logits"], workspace=dws, out=dout)
+        if fused:
+            binding.verify_and_confidence(inp["verify_logits"], rp, inp["draft_tokens"], inp["draft_logits"],
+                                          workspace=rws, out_verify=vout, out_draft=dout)
+        else:
+            binding.verify_accept(inp["verify_logits"], rp, inp["draft_tokens"], workspace=vws, out=vout)
+            binding.draft_confidence(inp["draft_logits"], workspace=dws, out=dout)
 
     step()
     torch.cuda.synchronize()

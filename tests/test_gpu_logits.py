@@ -148,3 +148,38 @@ def test_no_verify_rows_at_all():
     assert res["accept_len"].tolist() == [0, 0, 0]
     assert res["next_token"].tolist() == [-1, -1, -1]
     assert res["accept_entropy"].tolist() == [0.0, 0.0, 0.0]
+
+
+def _same(a, b):
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("case", ["tiny", "low", "high", "bonus_ties", "no_draft_rows", "empty_requests"])
+def test_fused_round_matches_separate_calls(case):
+    """rg_verify_and_confidence gives the two separate calls' results bit for
+    bit (same arithmetic, fewer launches), and so matches the oracle."""
+    if case == "bonus_ties":
+        lay = W.make_layout("mid", seed=8, num_requests=5, bonus_rows=True)
+        inp = W.make_logit_inputs(lay, DEV, ties=True)
+    elif case == "empty_requests":
+        lay = W.make_layout("high", seed=9, num_requests=7, verify=("choice", (0, 4), None))
+        inp = W.make_logit_inputs(lay, DEV)
+    else:
+        lay = W.make_layout("mid" if case == "no_draft_rows" else case, seed=7, num_requests=None if case != "no_draft_rows" else 3,
+                            draft=("fixed", 0) if case == "no_draft_rows" else None)
+        inp = W.make_logit_inputs(lay, DEV)
+    rp = torch.as_tensor(lay.row_indptr, device=DEV)
+    ws = binding.new_workspace(binding.verify_and_confidence_workspace_bytes(
+        lay.num_requests, lay.total_verify_rows, lay.total_draft_rows, lay.spec.vocab), DEV)
+    ws.fill_(0xFF)  # contents must not matter
+    fv, fd = binding.verify_and_confidence(inp["verify_logits"], rp, inp["draft_tokens"], inp["draft_logits"],
+                                           workspace=ws)
+    torch.cuda.synchronize()
+    sv = run_verify(lay, inp)
+    _same(sv, fv)
+    if lay.total_draft_rows:
+        sd = run_draft(inp["draft_logits"])
+        _same(sd, fd)
+        check_draft(inp["draft_logits"], fd)
+    check_verify(inp["verify_logits"], lay.row_indptr, inp["draft_tokens"], fv)
