@@ -19,7 +19,8 @@
 // log-sum-exp weights.
 //
 // K and V of 128 keys (8 pages) at a time are copied straight into LDS
-// (double buffered: the next buffer's copies are in flight while the current
+// (three K buffers and two V buffers: the next buffer's copies, and with
+// several key groups also the K after it, are in flight while the current
 // one is computed).  On each 32-key sub-tile a wave forms S^T = K Q^T with
 // v_mfma_f32_32x32x16_bf16 (K rows are the MFMA rows, query columns the MFMA
 // columns), applies the mask, updates the running max and sum in fp32 (exp2
@@ -133,7 +134,8 @@ constexpr int kWaves = 8;      // compute waves per work group (two per SIMD)
 constexpr int kProducers = 4;  // copy waves per work group (one per SIMD)
 constexpr int kThreads = 64 * (kWaves + kProducers);
 constexpr int kSuper = 128;  // keys staged per LDS buffer (four 32-key sub-tiles)
-constexpr int kBufs = 2;     // LDS buffers: one computed, one being filled
+constexpr int kKBufs = 3;    // K buffers: one computed, two being filled
+constexpr int kVBufs = 2;    // V buffers: one computed, one being filled
 static_assert(kSuper % kKeyTile == 0, "a super-tile is a whole number of key tiles");
 
 // Work group = 8 waves over (column tiles) x (key groups).  A request's
@@ -144,12 +146,11 @@ static_assert(kSuper % kKeyTile == 0, "a super-tile is a whole number of key til
 // (two per SIMD) busy on disjoint keys; the key groups' partial softmax
 // states are merged through LDS at the end.
 //
-// Keys stream through two LDS buffers of 128 keys (K and V of 8 pages).
-// While one buffer is computed the next one is filled by LDS-DMA; there is
-// one barrier per 128 keys.  The copies are issued by 4 dedicated waves (one
-// per SIMD): a CU accepts a 1 KiB LDS-DMA instruction only every few dozen
-// cycles, and a compute wave issuing its share would stall for most of a
-// buffer's worth of them instead of computing.
+// Keys stream through LDS 128 at a time (K and V of 8 pages), one barrier per
+// 128 keys.  The copies are issued by 4 dedicated waves (one per SIMD): a CU
+// accepts a 1 KiB LDS-DMA instruction only every few dozen cycles, and a
+// compute wave issuing its share would stall for most of a buffer's worth of
+// them instead of computing.
 template <int D>
 __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan p) {
   constexpr int NCH = D / 8;                   // 16-byte chunks per K row
@@ -163,12 +164,15 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   constexpr int MAXPAGES = kMaxChunkKeys / kPageSize;
   constexpr int COLS = 32 * kWaves;            // columns per column group
   static_assert(2 * BLOCKS % kProducers == 0 && BLOCKS == kProducers * (GP / 2), "DMA blocks split evenly");
-  static_assert(kBufs * SUPER * 2 * 2 >= (kWaves - 1) * (64 * 16 * DT + 128) * 4, "merge area");
+  static_assert((kKBufs + kVBufs) * SUPER * 2 >= (kWaves - 1) * (64 * 16 * DT + 128) * 4, "merge area");
 
-  // buf[b][0] = K of 128 keys ([key][D], 16-byte chunks swizzled per row),
-  // buf[b][1] = V of 8 pages ([page][D][16 keys], halves swizzled per row)
-  __shared__ __attribute__((aligned(16))) uint16_t buf[kBufs][2][SUPER];
-  __shared__ __attribute__((aligned(16))) int32_t lds_pages[MAXPAGES + kSuper / kPageSize];
+  // kbuf[b] = K of 128 keys ([key][D], 16-byte chunks swizzled per row),
+  // vbuf[b] = V of 8 pages ([page][D][16 keys], halves swizzled per row).
+  // K runs two buffers ahead and V one: a buffer's K is issued a whole
+  // buffer period before it is needed, with 160 KiB of LDS in all.
+  __shared__ __attribute__((aligned(16))) uint16_t lds[(kKBufs + kVBufs) * SUPER];
+  auto kbuf = [&](int s) { return lds + (s % kKBufs) * SUPER; };
+  auto vbuf = [&](int s) { return lds + (kKBufs + s % kVBufs) * SUPER; };
 
   const int item = xcd_item(p.grid_items);
   if (item >= p.total_items) return;
@@ -215,49 +219,53 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   int wave_min_lim = valid ? lim : kend;
   for (int off = 32; off >= 1; off >>= 1) wave_min_lim = min(wave_min_lim, __shfl_xor(wave_min_lim, off));
 
-  // Page indices of this chunk -> LDS (the one dependent round trip before the KV stream).
+  // Pages of this chunk: entries pg0 .. pg0 + npg - 1 of the request's list.
   const int pg0 = kbeg / kPageSize;
   const int npg = (kend + kPageSize - 1) / kPageSize - pg0;
-  for (int i = tid; i < npg; i += kThreads) lds_pages[i] = a.page_indices[rq.page_start + pg0 + i];
-  lds_barrier();
+  // The copy waves read page numbers through the scalar cache (uniform
+  // addresses in the constant address space): no LDS stage, no barrier.
+  typedef const int32_t __attribute__((address_space(4))) * cpage_ptr;
+  const cpage_ptr chunk_pages = (cpage_ptr)(a.page_indices + rq.page_start + pg0);
 
   const size_t head_stride = (size_t)kPageSize * D;  // elements per (page, head)
   const char* kbase_g = reinterpret_cast<const char*>(a.k_cache + (size_t)hk * head_stride);
   const char* vbase_g = reinterpret_cast<const char*>(a.v_cache + (size_t)hk * head_stride);
   const size_t page_bytes = (size_t)a.hkv * head_stride * 2;
 
-  // Copy wave pw issues blocks b = pw + 4 i of each buffer: the first GP / 2
-  // are K blocks (KPB keys each), the rest V blocks (32 head dims of a page).
-  // It first reads the page numbers of all its blocks (uniform LDS reads, one
-  // wait), then issues the transfers.  Page slots past the chunk's last page
-  // repeat that page, so buffer rows past the chunk end hold other tokens or
-  // unused slots of the last page (memory of the pool either way); their
-  // scores are masked and their values zeroed before use.
+  // Copy wave pw issues blocks b = pw + 4 i of each buffer's K (and of its
+  // V): KPB keys, or 32 head dims of one page, per 1 KiB block.  It reads the
+  // 8 page numbers of the buffer (one batch of scalar loads), then issues.
+  // Page slots past the chunk's last page repeat that page, so buffer rows
+  // past the chunk end hold other tokens or unused slots of the last page
+  // (memory of the pool either way); their scores are masked and their values
+  // zeroed before use.
   const int pw = wave - kWaves;
-  auto issue = [&](int s) {
+  auto read_pages = [&](int s, int (&pg)[kSuper / kPageSize]) {
     const int base = s * (kSuper / kPageSize);
-    int pg[GP];
 #pragma unroll
-    for (int i = 0; i < GP; ++i) {
+    for (int j = 0; j < kSuper / kPageSize; ++j) pg[j] = chunk_pages[min(base + j, npg - 1)];
+  };
+  auto issue_k = [&](int s) {
+    int pg[kSuper / kPageSize];
+    read_pages(s, pg);
+#pragma unroll
+    for (int i = 0; i < GP / 2; ++i) {
       const int b = pw + i * kProducers;  // wave-uniform
-      const int slot = i < GP / 2 ? (b * KPB) / kPageSize : (b - BLOCKS) / VBPP;
-      pg[i] = lds_pages[min(base + slot, npg - 1)];
+      const int kk = b * KPB + lane / NCH;
+      const uint32_t off = (uint32_t)((((kk % kPageSize) * D) + (((lane % NCH) ^ (swap23(kk & 31) & (NCH - 1))) * 8)) * 2);
+      dma16_s(kbase_g + (size_t)pg[(b * KPB) / kPageSize] * page_bytes, off,
+              (uint32_t)(uintptr_t)(kbuf(s) + b * 512));
     }
+  };
+  auto issue_v = [&](int s) {
+    int pg[kSuper / kPageSize];
+    read_pages(s, pg);
 #pragma unroll
-    for (int i = 0; i < GP; ++i) {
-      const int b = pw + i * kProducers;
-      uint32_t off, dst;
-      if (i < GP / 2) {
-        const int kk = b * KPB + lane / NCH;
-        off = (uint32_t)((((kk % kPageSize) * D) + (((lane % NCH) ^ (swap23(kk & 31) & (NCH - 1))) * 8)) * 2);
-        dst = (uint32_t)(uintptr_t)&buf[s & 1][0][b * 512];
-      } else {
-        const int d = ((b - BLOCKS) % VBPP) * 32 + (lane >> 1);
-        off = (uint32_t)((d * kPageSize + ((lane & 1) ^ vswz(d)) * 8) * 2);
-        dst = (uint32_t)(uintptr_t)&buf[s & 1][1][(b - BLOCKS) * 512];
-      }
-      dma16_s((i < GP / 2 ? kbase_g : vbase_g) + (size_t)__builtin_amdgcn_readfirstlane(pg[i]) * page_bytes, off,
-              dst);
+    for (int i = 0; i < GP / 2; ++i) {
+      const int b = pw + i * kProducers;  // V block of the buffer
+      const int d = (b % VBPP) * 32 + (lane >> 1);
+      const uint32_t off = (uint32_t)((d * kPageSize + ((lane & 1) ^ vswz(d)) * 8) * 2);
+      dma16_s(vbase_g + (size_t)pg[b / VBPP] * page_bytes, off, (uint32_t)(uintptr_t)(vbuf(s) + b * 512));
     }
   };
 
@@ -344,51 +352,71 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
     __builtin_amdgcn_sched_barrier(0);  // keep the next sub-tile's loads after this one's PV
   };
   const int nsup = (kend - kbeg + kSuper - 1) / kSuper;
-  // Plain loads (q) complete before the first LDS-DMA goes out: the compiler
-  // does not count the DMA instructions, and a q load it believed pending
-  // would make it wait for vmcnt(0) -- every copy in flight -- inside the loop.
-  if (producer) issue(0);
+  // Zero the values of keys past the chunk end in the last buffer (every
+  // wave takes part, so both loops below pass the same barriers), by 16-byte
+  // units (page slot pp, head dim d, half h = keys 16 pp + 8 h ..).
+  auto tail_fixup = [&](int s, int nvalid) {
+    uint16_t* vz = vbuf(s);
+    for (int u = tid; u < (kSuper / kPageSize) * D * 2; u += kThreads) {
+      const int pp = u / (2 * D), d = (u >> 1) % D, h = u & 1;
+      const int kfirst = kPageSize * pp + 8 * h;
+      if (kfirst + 8 <= nvalid) continue;
+      uint16_t* unit = vz + pp * (D * kPageSize) + d * kPageSize + ((h ^ vswz(d)) * 8);
+      if (kfirst >= nvalid) {
+        *(u32x4*)unit = u32x4{0u, 0u, 0u, 0u};
+      } else {
+        for (int e = nvalid - kfirst; e < 8; ++e) unit[e] = 0;
+      }
+    }
+    lds_barrier();
+  };
+
+  if (producer) {
+    // Deep mode (key groups > 1, where compute is short and the copies set the
+    // pace): K runs two buffers ahead.  Issue order K(0), V(0), K(1); then at
+    // buffer s: V(s + 1), K(s + 2), so when V(s) is complete only K(s + 1) can
+    // still be out.  Otherwise K and V of s + 1 go out together at buffer s.
+    const bool deep = kg > 1;
+    issue_k(0);
+    issue_v(0);
+    if (deep && nsup > 1) issue_k(1);
+    for (int s = 0; s < nsup; ++s) {
+      if (deep && s + 1 < nsup) wait_vmcnt<GP / 2>();  // this copy wave's K(s) and V(s)
+      else wait_vmcnt<0>();
+      lds_barrier();  // everyone's copies of buffer s are in; buffers of s - 1 are no longer read
+      const int nvalid = kend - (kbeg + s * kSuper);
+      if (nvalid < kSuper) tail_fixup(s, nvalid);
+      if (deep) {
+        if (s + 1 < nsup) issue_v(s + 1);  // into the V buffer of s - 1
+        if (s + 2 < nsup) issue_k(s + 2);  // into the K buffer of s - 1
+      } else if (s + 1 < nsup) {
+        issue_k(s + 1);  // into the K buffer of s - 2
+        issue_v(s + 1);  // into the V buffer of s - 1
+      }
+    }
+    return;
+  }
   for (int s = 0; s < nsup; ++s) {
-    if (producer) wait_vmcnt<0>();  // this copy wave's transfers of super-tile s
-    lds_barrier();  // everyone's: buffer s % 2 is full, buffer (s + 1) % 2 is no longer read
+    lds_barrier();
     const int k0 = kbeg + s * kSuper;
     const int nvalid = kend - k0;
-    const uint16_t* kt = buf[s & 1][0];
-    const uint16_t* vt = buf[s & 1][1];
-    if (nvalid < kSuper) {
-      // last buffer of the chunk: zero the values of keys past its end, by
-      // 16-byte units (page slot pp, head dim d, half h = keys 16 pp + 8 h ..)
-      uint16_t* vz = buf[s & 1][1];
-      for (int u = tid; u < (kSuper / kPageSize) * D * 2; u += kThreads) {
-        const int pp = u / (2 * D), d = (u >> 1) % D, h = u & 1;
-        const int kfirst = kPageSize * pp + 8 * h;
-        if (kfirst + 8 <= nvalid) continue;
-        uint16_t* unit = vz + pp * (D * kPageSize) + d * kPageSize + ((h ^ vswz(d)) * 8);
-        if (kfirst >= nvalid) {
-          *(u32x4*)unit = u32x4{0u, 0u, 0u, 0u};
-        } else {
-          for (int e = nvalid - kfirst; e < 8; ++e) unit[e] = 0;
-        }
-      }
-      lds_barrier();
-    }
-    if (producer) {
-      if (s + 1 < nsup) issue(s + 1);
-    } else if (tile_on) {
+    if (nvalid < kSuper) tail_fixup(s, nvalid);
+    if (tile_on) {
+      const uint16_t* kt = kbuf(s);
+      const uint16_t* vt = vbuf(s);
       // this wave's sub-tiles of the buffer: global sub-tile j = 4 s + q with j % kg == kgi
       for (int q = 0; q < kSuper / 32; ++q)
         if ((4 * s + q) % kg == kgi && 32 * q < nvalid) softmax_pv(qk(kt, q), k0 + 32 * q, vt, q);
     }
   }
 
-  if (producer) return;
 
   // Merge the key groups' partial states (lane-wise: same columns, same dims).
   // A wave's slot holds its accumulator as 16-byte rows, lane-interleaved.
   float l_tot = l_run + __shfl_xor(l_run, 32);
   if (kg > 1) {
     lds_barrier();  // every wave is done with the buffers before they are reused
-    float* area = reinterpret_cast<float*>(&buf[0][0][0]);
+    float* area = reinterpret_cast<float*>(lds);
     constexpr int PER = 64 * 16 * DT + 128;  // floats per wave slot
     if (tile_on && kgi > 0) {
       float* slot = area + (wave - nct2) * PER;
