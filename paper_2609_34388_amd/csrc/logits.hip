@@ -190,6 +190,7 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
     if (DRAFT) a2 = fmaxf(a2, fminf(a1, x[k]));
     a1 = fmaxf(a1, x[k]);
   }
+  const float own1 = a1, own2 = a2;  // this thread's largest two entries
   if (DRAFT) wave_top2(a1, a2);
   else a1 = wave_reduce(a1, [](float p, float q) { return fmaxf(p, q); });
   if (lane == 0) {
@@ -207,22 +208,28 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
   const float mc = m * kLog2e;
   const bool tail = v0 + kLogitChunk > v1;
   float zz = 0.f, ss = 0.f;
-  int cnt = 0, f1 = kNoIndex, f2 = kNoIndex, g = kNoIndex;
 #pragma unroll
-  for (int k = kE - 1; k >= 0; --k) {  // descending, so the lowest index is assigned last
-    const bool top = x[k] == m;
+  for (int k = 0; k < kE; ++k) {
     float t = __builtin_fmaf(x[k], kLog2e, -mc);
     if (tail) t = fmaxf(t, -1000.f);  // entries past the row end are -inf
-    const float e = top ? 0.f : __builtin_amdgcn_exp2f(t);
+    const float e = (x[k] == m) ? 0.f : __builtin_amdgcn_exp2f(t);
     zz += e;
     ss = __builtin_fmaf(e, t, ss);
-    cnt += top ? 1 : 0;
-    const int idx = entry_index(v0, k);
-    if (top) {
-      f2 = f1;
-      f1 = idx;
+  }
+  // Count and indices of the maximum (and, for draft rows, the first index of
+  // the runner-up value) only where this thread's own top two reach them:
+  // a few lanes per chunk, so the scan costs the chunk one short pass.
+  int cnt = 0, f1 = kNoIndex, f2 = kNoIndex, g = kNoIndex;
+  if (own1 == m || (DRAFT && v2 != kNegInf && (own1 == v2 || own2 == v2))) {
+    for (int k = kE - 1; k >= 0; --k) {  // descending, so the lowest index is assigned last
+      const int idx = entry_index(v0, k);
+      if (x[k] == m) {
+        ++cnt;
+        f2 = f1;
+        f1 = idx;
+      }
+      if (DRAFT && x[k] == v2) g = idx;
     }
-    if (DRAFT && x[k] == v2 && v2 != kNegInf) g = idx;
   }
   const auto add = [](float p, float q) { return p + q; };
   zz = wave_reduce(zz, add);
