@@ -208,13 +208,25 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
   const float mc = m * kLog2e;
   const bool tail = v0 + kLogitChunk > v1;
   float zz = 0.f, ss = 0.f;
+  // Entries equal to m are left out of Z''; only waves holding one compare.
+  if (__any(own1 == m)) {
 #pragma unroll
-  for (int k = 0; k < kE; ++k) {
-    float t = __builtin_fmaf(x[k], kLog2e, -mc);
-    if (tail) t = fmaxf(t, -1000.f);  // entries past the row end are -inf
-    const float e = (x[k] == m) ? 0.f : __builtin_amdgcn_exp2f(t);
-    zz += e;
-    ss = __builtin_fmaf(e, t, ss);
+    for (int k = 0; k < kE; ++k) {
+      float t = __builtin_fmaf(x[k], kLog2e, -mc);
+      if (tail) t = fmaxf(t, -1000.f);  // entries past the row end are -inf
+      const float e = (x[k] == m) ? 0.f : __builtin_amdgcn_exp2f(t);
+      zz += e;
+      ss = __builtin_fmaf(e, t, ss);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < kE; ++k) {
+      float t = __builtin_fmaf(x[k], kLog2e, -mc);
+      if (tail) t = fmaxf(t, -1000.f);
+      const float e = __builtin_amdgcn_exp2f(t);
+      zz += e;
+      ss = __builtin_fmaf(e, t, ss);
+    }
   }
   // Count and indices of the maximum (and, for draft rows, the first index of
   // the runner-up value) only where this thread's own top two reach them:
