@@ -115,7 +115,7 @@ rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
       if (nch > 1) {
         // partials are stored per 32-column tile, so columns round up to 32
         part += hkv * nch * round_up(M, 32);
-        comb += hkv * ((M + 31) / 32) * (L->head_dim / 16);  // 128-thread slices of a tile
+        comb += hkv * ((M + 31) / 32) * (L->head_dim / 32);  // 128-thread slices of a tile
         fp.split_requests += 1;
       }
       if (items > INT32_MAX / 2 || part > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
@@ -132,7 +132,7 @@ rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
     fp.total_partial_cols += part;
     fp.launches.push_back(p);
   }
-  const size_t o_bytes = align256((size_t)fp.max_partial_cols * L->head_dim * sizeof(float));
+  const size_t o_bytes = align256((size_t)fp.max_partial_cols * L->head_dim * sizeof(uint16_t));
   fp.ml_offset = o_bytes;
   fp.ws_bytes = fp.max_partial_cols ? o_bytes + align256((size_t)fp.max_partial_cols * 2 * sizeof(float)) : 0;
   return RG_OK;
@@ -214,7 +214,7 @@ rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t
   a.out = out;
   a.lse = lse;
   a.page_indices = layout->page_indices;
-  a.part_o = fp.ws_bytes ? static_cast<float*>(ws) : nullptr;
+  a.part_o = fp.ws_bytes ? static_cast<uint16_t*>(ws) : nullptr;
   a.part_ml = fp.ws_bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + fp.ml_offset) : nullptr;
   a.hq = layout->num_q_heads;
   a.hkv = layout->num_kv_heads;

@@ -467,30 +467,37 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
       }
     if (a.lse != nullptr && lh == 0) a.lse[orow] = m_run * a.sm_scale + __logf(l_tot);
   } else {
-    // Partial of this 32-column tile, stored in the accumulator's own order:
-    // 16-byte row (dt, ib) of lane l at ((dt * 4 + ib) * 64 + l) * 16 bytes,
-    // so every store instruction writes 1 KiB contiguously.
+    // Partial of this 32-column tile: the chunk's normalised output o / l in
+    // bf16 (with its fp32 max and sum beside it), stored in the accumulator's
+    // own order: 16-byte row (dt, j) of lane l (its registers 8 j .. 8 j + 7)
+    // at ((dt * 2 + j) * 64 + l) * 16 bytes, so every store instruction writes
+    // 1 KiB contiguously.
     const int M32 = (M + 31) & ~31;
     const size_t tile0 = (size_t)rq.part_start + ((size_t)hk * nch + c) * M32 + (size_t)(cg * COLS + ct * 32);
-    float* dst = a.part_o + tile0 * D;
+    uint16_t* dst = a.part_o + tile0 * D;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;  // 0: no key of this chunk is visible to the column
     for (int dt = 0; dt < DT; ++dt)
-      for (int ib = 0; ib < 4; ++ib)
-        *(float4*)(dst + ((dt * 4 + ib) * 64 + lane) * 4) =
-            make_float4(acc[dt][4 * ib + 0], acc[dt][4 * ib + 1], acc[dt][4 * ib + 2], acc[dt][4 * ib + 3]);
+      for (int j = 0; j < 2; ++j) {
+        u32x4 w;
+        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(acc[dt][8 * j + 2 * e] * inv, acc[dt][8 * j + 2 * e + 1] * inv);
+        *(u32x4*)(dst + ((dt * 2 + j) * 64 + lane) * 8) = w;
+      }
     if (lh == 0) *(float2*)(a.part_ml + 2 * (tile0 + lc)) = make_float2(m_run, l_tot);
   }
 }
 
 // Merge of the split-KV partials.  Work item = (request, KV head, 32-column
 // tile, slice of 128 16-byte rows of the tile's fragment-ordered block); a
-// thread owns one row (4 head dims of one column), reads that row and its
-// column's (max, sum) from every chunk -- eight chunks' loads in flight at a
-// time -- merges them with online rescaling and writes 4 bf16 outputs.
+// thread owns one row (8 head dims of one column: two runs of 4), reads that
+// row and its column's (max, sum) from every chunk -- eight chunks' loads in
+// flight at a time -- merges them with online rescaling (chunk weight
+// exp(m_c - m) * l_c on the chunk's normalised output) and writes 8 bf16
+// outputs.
 constexpr int kCombThreads = 128;
 
 template <int D>
 __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnArgs a, AttnPlan p) {
-  constexpr int SLICES = 8 * D / kCombThreads;  // 16-byte rows per tile block / threads
+  constexpr int SLICES = 4 * D / kCombThreads;  // 16-byte rows per tile block / threads
   const int item = xcd_item(p.grid_comb);
   if (item >= p.total_comb) return;
   const int r = find_request(p, item, true);
@@ -510,18 +517,19 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnArgs a, 
   const size_t base = (size_t)rq.part_start + (size_t)hk * nch * M32 + (size_t)tile * 32;
 
   float m = kNegInf, l = 0.f;
-  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  float o[8];
+  for (int e = 0; e < 8; ++e) o[e] = 0.f;
   for (int c0 = 0; c0 < nch; c0 += 8) {
     float2 ml[8];
-    float4 v[8];
+    u32x4 v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       ml[u] = make_float2(kNegInf, 0.f);
-      v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      v[u] = u32x4{0u, 0u, 0u, 0u};
       if (c0 + u < nch) {
         const size_t t0 = base + (size_t)(c0 + u) * M32;
         ml[u] = *(const float2*)(a.part_ml + 2 * (t0 + lc));
-        v[u] = *(const float4*)(a.part_o + t0 * D + (size_t)f * 4);
+        v[u] = *(const u32x4*)(a.part_o + t0 * D + (size_t)f * 8);
       }
     }
 #pragma unroll
@@ -529,12 +537,13 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnArgs a, 
       if (ml[u].x == kNegInf) continue;  // no key of that chunk is visible to this column
       const float m_new = fmaxf(m, ml[u].x);
       const float a0 = __builtin_amdgcn_exp2f((m - m_new) * a.scale_log2);
-      const float a1 = __builtin_amdgcn_exp2f((ml[u].x - m_new) * a.scale_log2);
-      l = l * a0 + ml[u].y * a1;
-      o.x = o.x * a0 + v[u].x * a1;
-      o.y = o.y * a0 + v[u].y * a1;
-      o.z = o.z * a0 + v[u].z * a1;
-      o.w = o.w * a0 + v[u].w * a1;
+      const float a1 = __builtin_amdgcn_exp2f((ml[u].x - m_new) * a.scale_log2) * ml[u].y;
+      l = l * a0 + a1;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        o[2 * e] = o[2 * e] * a0 + __uint_as_float(v[u][e] << 16) * a1;
+        o[2 * e + 1] = o[2 * e + 1] * a0 + __uint_as_float(v[u][e] & 0xffff0000u) * a1;
+      }
       m = m_new;
     }
   }
@@ -544,11 +553,14 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnArgs a, 
   const int hh = gc - tok * g;
   const size_t orow = (size_t)(rq.q_start + tok) * a.hq + hk * g + hh;
   const float inv = 1.f / l;
-  const int d0 = 32 * (q >> 2) + 8 * (q & 3) + 4 * lh;
-  u32x2 w;
-  w[0] = pack_bf16x2(o.x * inv, o.y * inv);
-  w[1] = pack_bf16x2(o.z * inv, o.w * inv);
-  *(u32x2*)(a.out + orow * D + d0) = w;
+  const int d0 = 32 * (q >> 1) + 16 * (q & 1) + 4 * lh;  // dims d0 .. d0 + 3 and d0 + 8 .. d0 + 11
+  u32x2 w0, w1;
+  w0[0] = pack_bf16x2(o[0] * inv, o[1] * inv);
+  w0[1] = pack_bf16x2(o[2] * inv, o[3] * inv);
+  w1[0] = pack_bf16x2(o[4] * inv, o[5] * inv);
+  w1[1] = pack_bf16x2(o[6] * inv, o[7] * inv);
+  *(u32x2*)(a.out + orow * D + d0) = w0;
+  *(u32x2*)(a.out + orow * D + d0 + 8) = w1;
   if (a.lse != nullptr && f < 32) a.lse[orow] = m * a.sm_scale + __logf(l);
 }
 

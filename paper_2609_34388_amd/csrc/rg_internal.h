@@ -48,7 +48,7 @@ struct AttnArgs {
   uint16_t* out;
   float* lse;
   const int32_t* page_indices;
-  float* part_o;   // per 32-column tile: 32 x D fp32 un-normalised, in MFMA fragment order
+  uint16_t* part_o;  // per 32-column tile: 32 x D bf16 normalised partial outputs, MFMA fragment order
   float* part_ml;  // [partial columns][2] fp32 (running max of raw scores, sum)
   int32_t hq, hkv, g;
   float sm_scale;    // natural-log domain scale
