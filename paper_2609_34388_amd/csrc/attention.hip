@@ -138,13 +138,12 @@ constexpr int kKBufs = 3;    // K buffers: one computed, two being filled
 constexpr int kVBufs = 2;    // V buffers: one computed, one being filled
 static_assert(kSuper % kKeyTile == 0, "a super-tile is a whole number of key tiles");
 
-// Work group = 8 waves over (column tiles) x (key groups).  A request's
-// columns are split into groups of up to 256; a group of nct 32-column tiles
-// uses nct' = nct rounded up to a power of two tiles and kg = 8 / nct' key
-// groups: wave w handles column tile w % nct' and the 32-key sub-tiles j of
-// the chunk with j % kg == w / nct'.  Small requests thus keep all 8 waves
-// (two per SIMD) busy on disjoint keys; the key groups' partial softmax
-// states are merged through LDS at the end.
+// Work group = 8 compute waves over (column tiles) x (key groups).  A
+// request's columns are split into groups of up to 256 (8 tiles of 32); a
+// wave handling key group kgi of kg processes the chunk's 32-key sub-tiles j
+// with j % kg == kgi.  Small requests thus keep all 8 waves (two per SIMD)
+// busy on disjoint keys; the key groups' partial softmax states are merged
+// through LDS at the end.
 //
 // Keys stream through LDS 128 at a time (K and V of 8 pages), one barrier per
 // 128 keys.  The copies are issued by 4 dedicated waves (one per SIMD): a CU
@@ -164,7 +163,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   constexpr int MAXPAGES = kMaxChunkKeys / kPageSize;
   constexpr int COLS = 32 * kWaves;            // columns per column group
   static_assert(2 * BLOCKS % kProducers == 0 && BLOCKS == kProducers * (GP / 2), "DMA blocks split evenly");
-  static_assert((kKBufs + kVBufs) * SUPER * 2 >= (kWaves - 1) * (64 * 16 * DT + 128) * 4, "merge area");
+  static_assert((kKBufs + kVBufs) * SUPER * 2 >= kWaves * (64 * 16 * DT + 128) * 4, "merge area");
 
   // kbuf[b] = K of 128 keys ([key][D], 16-byte chunks swizzled per row),
   // vbuf[b] = V of 8 pages ([page][D][16 keys], halves swizzled per row).
@@ -195,12 +194,37 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, in an SGPR
   const int lc = lane & 31, lh = lane >> 5;
 
-  // column tiles of this group and the wave's (column tile, key group)
+  // Column tiles of this group and each compute wave's (column tile ct, key
+  // group kgi of kg; the tile's other key groups are waves w + k kstride).
+  // Compute waves w and w + 4 share a SIMD.  Up to 4 tiles: every tile gets
+  // 8 / nct' waves (nct' = nct rounded up to a power of two).  5 to 7 tiles:
+  // tiles 0-3 get waves 0-3 and the rest share waves 4-7 by key groups, so
+  // no SIMD carries two whole tiles while another idles.
   const int nct = min(kWaves, (M - cg * COLS + 31) / 32);
-  const int nct2 = nct <= 1 ? 1 : nct <= 2 ? 2 : nct <= 4 ? 4 : 8;
-  const int kg = kWaves / nct2;
   const bool producer = wave >= kWaves;  // wave-uniform: copy wave
-  const int ct = wave % nct2, kgi = wave / nct2;
+  int ct, kg, kgi, kstride;
+  if (nct <= 4) {
+    const int nct2 = nct <= 1 ? 1 : nct <= 2 ? 2 : 4;
+    ct = wave % nct2;
+    kg = kWaves / nct2;
+    kgi = wave / nct2;
+    kstride = nct2;
+  } else if (wave < 4 || nct == 8) {
+    ct = wave;
+    kg = 1;
+    kgi = 0;
+    kstride = 1;
+  } else if (nct == 7) {  // tiles 4, 5 on waves 4, 5; tile 6 on waves 6, 7
+    ct = min(wave, 6);
+    kg = wave < 6 ? 1 : 2;
+    kgi = wave < 6 ? 0 : wave - 6;
+    kstride = 1;
+  } else {  // 5 tiles: tile 4 on waves 4-7; 6 tiles: tile 4 on 4, 5 and tile 5 on 6, 7
+    kg = 4 / (nct - 4);
+    ct = 4 + (wave - 4) / kg;
+    kgi = (wave - 4) % kg;
+    kstride = 1;
+  }
   const bool tile_on = !producer && ct < nct;  // wave-uniform
   const int col = cg * COLS + ct * 32 + lc;
   const bool valid = tile_on && col < M;
@@ -376,7 +400,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
     // pace): K runs two buffers ahead.  Issue order K(0), V(0), K(1); then at
     // buffer s: V(s + 1), K(s + 2), so when V(s) is complete only K(s + 1) can
     // still be out.  Otherwise K and V of s + 1 go out together at buffer s.
-    const bool deep = kg > 1;
+    const bool deep = nct <= 4;  // every tile split over key groups
     issue_k(0);
     issue_v(0);
     if (deep && nsup > 1) issue_k(1);
@@ -406,7 +430,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
       const uint16_t* vt = vbuf(s);
       // this wave's sub-tiles of the buffer: global sub-tile j = 4 s + q with j % kg == kgi
       for (int q = 0; q < kSuper / 32; ++q)
-        if ((4 * s + q) % kg == kgi && 32 * q < nvalid) softmax_pv(qk(kt, q), k0 + 32 * q, vt, q);
+        if (((4 * s + q) & (kg - 1)) == kgi && 32 * q < nvalid) softmax_pv(qk(kt, q), k0 + 32 * q, vt, q);
     }
   }
 
@@ -414,12 +438,12 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   // Merge the key groups' partial states (lane-wise: same columns, same dims).
   // A wave's slot holds its accumulator as 16-byte rows, lane-interleaved.
   float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (kg > 1) {
+  if (nct < 8) {  // some tile is split over key groups (uniform: every compute wave passes the barriers)
     lds_barrier();  // every wave is done with the buffers before they are reused
     float* area = reinterpret_cast<float*>(lds);
     constexpr int PER = 64 * 16 * DT + 128;  // floats per wave slot
     if (tile_on && kgi > 0) {
-      float* slot = area + (wave - nct2) * PER;
+      float* slot = area + wave * PER;
       for (int dt = 0; dt < DT; ++dt)
         for (int ib = 0; ib < 4; ++ib)
           *(float4*)(slot + ((dt * 4 + ib) * 64 + lane) * 4) =
@@ -430,7 +454,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
     lds_barrier();
     if (!tile_on || kgi > 0) return;
     for (int k = 1; k < kg; ++k) {
-      const float* slot = area + (k * nct2 + ct - nct2) * PER;
+      const float* slot = area + (wave + k * kstride) * PER;
       const float mk = slot[64 * 16 * DT + lane];
       if (mk == kNegInf) continue;
       const float lk = slot[64 * 16 * DT + 64 + lane];

@@ -92,7 +92,10 @@ def test_scaled_down_configs_full(kind, seed):
     dict(ctx=[50], nv=[7], nd=[0]),                      # verify rows only
     dict(ctx=[0], nv=[0], nd=[1]),                       # one key
     dict(ctx=[5], nv=[1], nd=[0]),                       # T < page
-    dict(ctx=[300], nv=[16], nd=[24]),                   # 160 columns: two tiles per wave
+    dict(ctx=[300], nv=[16], nd=[24]),                   # 160 columns: 5 tiles, the 5th over 4 key groups
+    dict(ctx=[530], nv=[20], nd=[24]),                   # 176 columns: 6 tiles
+    dict(ctx=[410], nv=[24], nd=[28]),                   # 208 columns: 7 tiles
+    dict(ctx=[260], nv=[32], nd=[32]),                   # 256 columns: 8 tiles, no key groups
     dict(ctx=[129], nv=[32], nd=[38]),                   # 280 columns: two column groups
     dict(ctx=[64, 0, 200], nv=[4, 0, 9], nd=[4, 0, 7]),  # an empty request in the middle
     dict(ctx=[1000], nv=[2], nd=[2], hq=4, hkv=4),       # g = 1
