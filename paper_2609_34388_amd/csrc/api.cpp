@@ -59,19 +59,44 @@ struct FullPlan {
   size_t ml_offset = 0;
 };
 
-// Keys per work item: enough items to cover the 256 CUs a few times over,
-// but no smaller than the floor (small chunks multiply the partial outputs a
-// split request writes and re-reads: columns * D * 4 bytes per chunk against
-// chunk * D * 4 bytes of K/V).
-int choose_chunk(int64_t total_keys) {
+// Keys per work item.  An item costs a fixed start-up and wind-down (request
+// lookup, page numbers, first copies, epilogue) besides its keys, and
+// splitting a request adds partial outputs and the combine kernel; items are
+// dispatched longest request first.  `pair_keys` holds T of every (request,
+// KV head, column group); with S = sum / 256 (one CU's share of the keys):
+//  - no split when the pairs alone give three items per CU and none exceeds
+//    S / 2 (the longest-first order then balances them);
+//  - otherwise the longest chunk (a multiple of the LDS buffer) that keeps
+//    every item within S / 4 and gives at least two items per CU, but no
+//    shorter than 256 keys.
+int choose_chunk(const std::vector<int64_t>& pair_keys) {
   const int forced = env_int("RG_ATTN_CHUNK", 0);
   if (forced > 0) return (int)std::min<int64_t>(kMaxChunkKeys, round_up(forced, kKeyTile));
-  const int target = std::max(1, env_int("RG_ATTN_TARGET_ITEMS", 1024));
-  const int floor_keys = std::max(kKeyTile, env_int("RG_ATTN_MIN_CHUNK", 256));
-  int64_t chunk = round_up((total_keys + target - 1) / target, kKeyTile);
-  chunk = std::max<int64_t>(chunk, round_up(floor_keys, kKeyTile));
-  chunk = std::min<int64_t>(chunk, kMaxChunkKeys);
-  return (int)chunk;
+  constexpr int64_t kCUs = 256;
+  const int64_t floor_keys = round_up(std::max(kKeyTile, env_int("RG_ATTN_MIN_CHUNK", 256)), kKeyTile);
+  int64_t total = 0, longest = 0;
+  for (int64_t t : pair_keys) {
+    total += t;
+    longest = std::max(longest, t);
+  }
+  const int64_t share = total / kCUs;
+  const int64_t whole = std::min<int64_t>(kMaxChunkKeys, std::max(floor_keys, round_up(longest, kKeyTile)));
+  if ((int64_t)pair_keys.size() >= 3 * kCUs && longest <= share / 2) return (int)whole;
+  auto items = [&](int64_t chunk) {
+    int64_t n = 0;
+    for (int64_t t : pair_keys) n += (t + chunk - 1) / chunk;
+    return n;
+  };
+  int64_t hi = std::min(whole, std::max(floor_keys, round_up(share / 4, kKeyTile)));
+  int64_t lo = floor_keys;
+  if (items(lo) < 2 * kCUs) return (int)lo;
+  while (lo < hi) {  // invariant: items(lo) >= 2 * kCUs
+    const int64_t mid = round_up((lo + hi + 1) / 2, kKeyTile);
+    if (mid > hi) break;
+    if (items(mid) >= 2 * kCUs) lo = mid;
+    else hi = mid - kKeyTile;
+  }
+  return (int)lo;
 }
 
 rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
@@ -79,14 +104,22 @@ rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
   const int g = L->num_q_heads / L->num_kv_heads;
   const int hkv = L->num_kv_heads;
   fp.cols_per_group = 256;  // 8 waves x 32 columns per work group
-  int64_t total_keys = 0;
+  std::vector<int64_t> pair_keys;
   for (int r = 0; r < R; ++r) {
     const int64_t n = L->q_indptr[r + 1] - L->q_indptr[r];
     if (n == 0) continue;
     const int64_t ncg = (n * g + fp.cols_per_group - 1) / fp.cols_per_group;
-    total_keys += ((int64_t)L->ctx_len[r] + n) * hkv * ncg;
+    for (int64_t k = 0; k < hkv * ncg; ++k) pair_keys.push_back((int64_t)L->ctx_len[r] + n);
   }
-  fp.chunk = choose_chunk(total_keys);
+  fp.chunk = choose_chunk(pair_keys);
+  // Longest requests first: work groups are dispatched in item order, so the
+  // long items start early and the short ones fill in at the end.
+  std::vector<int> order(R);
+  for (int r = 0; r < R; ++r) order[r] = r;
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+    return (int64_t)L->ctx_len[x] + (L->q_indptr[x + 1] - L->q_indptr[x]) >
+           (int64_t)L->ctx_len[y] + (L->q_indptr[y + 1] - L->q_indptr[y]);
+  });
   for (int r0 = 0; r0 < R; r0 += kMaxReqPerLaunch) {
     const int cnt = std::min(kMaxReqPerLaunch, R - r0);
     AttnPlan p;
@@ -96,7 +129,7 @@ rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
     p.cols_per_group = fp.cols_per_group;
     int64_t items = 0, part = 0, comb = 0;
     for (int k = 0; k < cnt; ++k) {
-      const int r = r0 + k;
+      const int r = order[r0 + k];
       const int64_t n = L->q_indptr[r + 1] - L->q_indptr[r];
       AttnReq& q = p.req[k];
       q.q_start = L->q_indptr[r];

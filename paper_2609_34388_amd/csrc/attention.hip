@@ -160,7 +160,6 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   constexpr int KPB = 1024 / (2 * D);          // keys per K block
   constexpr int VBPP = D / 32;                 // V blocks per page
   constexpr int GP = 2 * BLOCKS / kProducers;  // DMA instructions per copy wave per buffer
-  constexpr int MAXPAGES = kMaxChunkKeys / kPageSize;
   constexpr int COLS = 32 * kWaves;            // columns per column group
   static_assert(2 * BLOCKS % kProducers == 0 && BLOCKS == kProducers * (GP / 2), "DMA blocks split evenly");
   static_assert((kKBufs + kVBufs) * SUPER * 2 >= kWaves * (64 * 16 * DT + 128) * 4, "merge area");
@@ -173,7 +172,10 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   auto kbuf = [&](int s) { return lds + (s % kKBufs) * SUPER; };
   auto vbuf = [&](int s) { return lds + (kKBufs + s % kVBufs) * SUPER; };
 
-  const int item = xcd_item(p.grid_items);
+  // One request: its heads' chunk ranges go to one XCD each (shared q and
+  // page list in that XCD's L2).  Several: dispatch order, so the longest
+  // requests, which come first, spread over all XCDs.
+  const int item = p.num_req == 1 ? xcd_item(p.grid_items) : (int)blockIdx.x;
   if (item >= p.total_items) return;
   const int r = find_request(p, item, false);
   const AttnReq rq = p.req[r];

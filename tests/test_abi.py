@@ -125,7 +125,7 @@ def test_plan_accounting(name):
     info = _plan(l)
     g = s.num_q_heads // s.num_kv_heads
     ch = info.chunk_keys
-    assert ch % 128 == 0 and 128 <= ch <= 8192
+    assert ch % 128 == 0 and 128 <= ch <= 65536
     cpg = 256
     items = split = part = 0
     for r in range(lay.num_requests):
