@@ -84,24 +84,11 @@ __device__ __forceinline__ int xcd_item(int grid_items) {
 }
 
 // Direct global -> LDS copy of 16 bytes per lane (LDS-DMA).  The wave's 64
-// lanes fill 1 KiB of LDS starting at `lds_byte_addr` (lane L at +16 L).
-// Issued through inline assembly so that the compiler does not insert a
-// wait for every outstanding copy before each LDS read; the kernel waits on
-// the vector-memory counter itself.  m0 is saved and restored around it.
-__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_byte_addr) {
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %1\n\t"
-      "global_load_lds_dwordx4 %2, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(__builtin_amdgcn_readfirstlane(lds_byte_addr)), "v"(gptr)
-      : "memory");
-}
-
-// Same with a wave-uniform 64-bit base in SGPRs and a per-lane 32-bit byte
-// offset (the saddr form: no per-lane 64-bit address arithmetic).
+// lanes fill 1 KiB of LDS starting at `lds_byte_addr` (lane L at +16 L); the
+// source is a wave-uniform 64-bit base in SGPRs plus a per-lane 32-bit byte
+// offset.  Issued through inline assembly so that the compiler does not
+// insert a wait for every outstanding copy before each LDS read; the kernel
+// waits on the vector-memory counter itself.  m0 is saved and restored.
 __device__ __forceinline__ void dma16_s(const void* sbase, uint32_t voff, uint32_t lds_byte_addr) {
   uint32_t saved;
   asm volatile(

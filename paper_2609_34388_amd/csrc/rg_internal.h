@@ -13,7 +13,6 @@ constexpr int kPageSize = 16;
 constexpr int kMaxReqPerLaunch = 128;  // equals RG_ATTN_MAX_REQS_PER_LAUNCH
 constexpr int kKeyTile = 128;          // keys per LDS buffer; chunks are multiples of it
 constexpr int kMaxChunkKeys = 1 << 16;  // keys per work item at most
-constexpr int kAttnThreads = 256;      // 4 waves of 64
 
 // Per-request data of one attention launch.  Everything a work group needs
 // about its request travels in the kernel arguments, so no table has to be
