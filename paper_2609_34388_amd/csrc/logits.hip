@@ -163,6 +163,39 @@ __device__ __forceinline__ void wave_min2(int& v1, int& v2) {
   v2 = a2;
 }
 
+// Z'' and S partial sums of this thread's entries: exp(x - m) over entries
+// below m (all entries when EXCLUDE is false: the caller knows none equals
+// m), and exp(x - m)(x - m) in log2 units.  Entries past the row end are -inf
+// and only occur in a row's last chunk (TAIL), where t is clamped so that
+// e * t stays 0.  Two independent accumulator chains halve the dependent
+// latency.
+template <bool TAIL, bool EXCLUDE>
+__device__ __forceinline__ void exp_sums(const float (&x)[kE], float m, float& zz, float& ss) {
+  const float mc = m * kLog2e;
+  float z0 = 0.f, z1 = 0.f, s0 = 0.f, s1 = 0.f;
+#pragma unroll
+  for (int k = 0; k < kE; k += 2) {
+    float t0 = __builtin_fmaf(x[k], kLog2e, -mc);
+    float t1 = __builtin_fmaf(x[k + 1], kLog2e, -mc);
+    if (TAIL) {
+      t0 = fmaxf(t0, -1000.f);
+      t1 = fmaxf(t1, -1000.f);
+    }
+    float e0 = __builtin_amdgcn_exp2f(t0);
+    float e1 = __builtin_amdgcn_exp2f(t1);
+    if (EXCLUDE) {
+      e0 = (x[k] == m) ? 0.f : e0;
+      e1 = (x[k + 1] == m) ? 0.f : e1;
+    }
+    z0 += e0;
+    z1 += e1;
+    s0 = __builtin_fmaf(e0, t0, s0);
+    s1 = __builtin_fmaf(e1, t1, s1);
+  }
+  zz = z0 + z1;
+  ss = s0 + s1;
+}
+
 struct ChunkRed {
   float top[2][4];  // per wave: largest, second largest value
   float zs[2][4];   // per wave: Z'' and S partial sums
@@ -184,13 +217,28 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
   float x[kE];
   load_chunk(row, v0, v1, vec, x);
 
-  float a1 = kNegInf, a2 = kNegInf;
+  // This thread's largest two entries, over two independent chains (even and
+  // odd entry pairs).  With a1 >= a2, the runner-up after adding x is the
+  // median of (a1, a2, x).
+  float a1 = kNegInf, a2 = kNegInf, b1 = kNegInf, b2 = kNegInf;
 #pragma unroll
-  for (int k = 0; k < kE; ++k) {
-    if (DRAFT) a2 = fmaxf(a2, fminf(a1, x[k]));
-    a1 = fmaxf(a1, x[k]);
+  for (int k = 0; k < kE; k += 4) {
+    if (DRAFT) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        a2 = __builtin_amdgcn_fmed3f(a1, a2, x[k + j]);
+        a1 = fmaxf(a1, x[k + j]);
+        b2 = __builtin_amdgcn_fmed3f(b1, b2, x[k + 2 + j]);
+        b1 = fmaxf(b1, x[k + 2 + j]);
+      }
+    } else {
+      a1 = fmaxf(a1, fmaxf(x[k], x[k + 1]));
+      b1 = fmaxf(b1, fmaxf(x[k + 2], x[k + 3]));
+    }
   }
-  const float own1 = a1, own2 = a2;  // this thread's largest two entries
+  if (DRAFT) top2_merge(a1, a2, b1, b2);
+  else a1 = fmaxf(a1, b1);
+  const float own1 = a1, own2 = a2;
   if (DRAFT) wave_top2(a1, a2);
   else a1 = wave_reduce(a1, [](float p, float q) { return fmaxf(p, q); });
   if (lane == 0) {
@@ -205,28 +253,15 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
     else m = fmaxf(m, red.top[0][w]);
   }
 
-  const float mc = m * kLog2e;
-  const bool tail = v0 + kLogitChunk > v1;
-  float zz = 0.f, ss = 0.f;
   // Entries equal to m are left out of Z''; only waves holding one compare.
-  if (__any(own1 == m)) {
-#pragma unroll
-    for (int k = 0; k < kE; ++k) {
-      float t = __builtin_fmaf(x[k], kLog2e, -mc);
-      if (tail) t = fmaxf(t, -1000.f);  // entries past the row end are -inf
-      const float e = (x[k] == m) ? 0.f : __builtin_amdgcn_exp2f(t);
-      zz += e;
-      ss = __builtin_fmaf(e, t, ss);
-    }
+  float zz, ss;
+  const bool exclude = __any(own1 == m);
+  if (v0 + kLogitChunk <= v1) {
+    if (exclude) exp_sums<false, true>(x, m, zz, ss);
+    else exp_sums<false, false>(x, m, zz, ss);
   } else {
-#pragma unroll
-    for (int k = 0; k < kE; ++k) {
-      float t = __builtin_fmaf(x[k], kLog2e, -mc);
-      if (tail) t = fmaxf(t, -1000.f);
-      const float e = __builtin_amdgcn_exp2f(t);
-      zz += e;
-      ss = __builtin_fmaf(e, t, ss);
-    }
+    if (exclude) exp_sums<true, true>(x, m, zz, ss);
+    else exp_sums<true, false>(x, m, zz, ss);
   }
   // Count and indices of the maximum (and, for draft rows, the first index of
   // the runner-up value) only where this thread's own top two reach them:
