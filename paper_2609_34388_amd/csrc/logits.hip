@@ -217,28 +217,40 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
   float x[kE];
   load_chunk(row, v0, v1, vec, x);
 
-  // This thread's largest two entries, over two independent chains (even and
-  // odd entry pairs).  With a1 >= a2, the runner-up after adding x is the
-  // median of (a1, a2, x).
-  float a1 = kNegInf, a2 = kNegInf, b1 = kNegInf, b2 = kNegInf;
+  // Maximum of each group of 8 entries (one 16-byte load: consecutive
+  // vocabulary indices) and this thread's largest entry; for draft rows also
+  // each group's and the thread's runner-up.  Groups are independent chains;
+  // with t1 >= t2, the runner-up after adding x is the median of (t1, t2, x).
+  float gm[kU];
+  float a1, a2 = kNegInf;
+  if (DRAFT) {
+    float g2[kU];
 #pragma unroll
-  for (int k = 0; k < kE; k += 4) {
-    if (DRAFT) {
+    for (int u = 0; u < kU; ++u) {
+      float t1 = kNegInf, t2 = kNegInf;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        a2 = __builtin_amdgcn_fmed3f(a1, a2, x[k + j]);
-        a1 = fmaxf(a1, x[k + j]);
-        b2 = __builtin_amdgcn_fmed3f(b1, b2, x[k + 2 + j]);
-        b1 = fmaxf(b1, x[k + 2 + j]);
+      for (int j = 0; j < 8; ++j) {
+        t2 = __builtin_amdgcn_fmed3f(t1, t2, x[8 * u + j]);
+        t1 = fmaxf(t1, x[8 * u + j]);
       }
-    } else {
-      a1 = fmaxf(a1, fmaxf(x[k], x[k + 1]));
-      b1 = fmaxf(b1, fmaxf(x[k + 2], x[k + 3]));
+      gm[u] = t1;
+      g2[u] = t2;
     }
+    a1 = gm[0];
+    a2 = g2[0];
+#pragma unroll
+    for (int u = 1; u < kU; ++u) top2_merge(a1, a2, gm[u], g2[u]);
+  } else {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const float* y = x + 8 * u;
+      gm[u] = fmaxf(fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])), fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7])));
+    }
+    a1 = gm[0];
+#pragma unroll
+    for (int u = 1; u < kU; ++u) a1 = fmaxf(a1, gm[u]);
   }
-  if (DRAFT) top2_merge(a1, a2, b1, b2);
-  else a1 = fmaxf(a1, b1);
-  const float own1 = a1, own2 = a2;
+  const float own1 = a1;
   if (DRAFT) wave_top2(a1, a2);
   else a1 = wave_reduce(a1, [](float p, float q) { return fmaxf(p, q); });
   if (lane == 0) {
@@ -264,30 +276,41 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
     else exp_sums<true, false>(x, m, zz, ss);
   }
   // Count and indices of the maximum (and, for draft rows, the first index of
-  // the runner-up value) only where this thread's own top two reach them:
-  // a few lanes per chunk, so the scan costs the chunk one short pass.
+  // the runner-up value): only groups whose maximum reaches m (or v2) can hold
+  // them -- usually one group of one lane per chunk -- so only those groups
+  // are scanned, and only waves that scanned reduce the results.
+  const bool has_v2 = DRAFT && v2 != kNegInf;
+  const float thr = has_v2 ? v2 : m;  // v2 <= m
   int cnt = 0, f1 = kNoIndex, f2 = kNoIndex, g = kNoIndex;
-  if (own1 == m || (DRAFT && v2 != kNegInf && (own1 == v2 || own2 == v2))) {
-    for (int k = kE - 1; k >= 0; --k) {  // descending, so the lowest index is assigned last
-      const int idx = entry_index(v0, k);
-      if (x[k] == m) {
-        ++cnt;
-        f2 = f1;
-        f1 = idx;
+  bool scanned = false;
+#pragma unroll
+  for (int u = kU - 1; u >= 0; --u) {  // descending, so the lowest index is assigned last
+    if (gm[u] >= thr) {
+      scanned = true;
+#pragma unroll
+      for (int j = 7; j >= 0; --j) {
+        const int idx = entry_index(v0, 8 * u + j);
+        if (x[8 * u + j] == m) {
+          ++cnt;
+          f2 = f1;
+          f1 = idx;
+        }
+        if (has_v2 && x[8 * u + j] == v2) g = idx;
       }
-      if (DRAFT && x[k] == v2) g = idx;
     }
   }
   const auto add = [](float p, float q) { return p + q; };
   zz = wave_reduce(zz, add);
   ss = wave_reduce(ss, add);
-  cnt = wave_reduce(cnt, [](int p, int q) { return p + q; });
-  const auto imin = [](int p, int q) { return min(p, q); };
-  if (DRAFT) {
-    wave_min2(f1, f2);
-    g = wave_reduce(g, imin);
-  } else {
-    f1 = wave_reduce(f1, imin);
+  if (__any(scanned)) {
+    cnt = wave_reduce(cnt, [](int p, int q) { return p + q; });
+    const auto imin = [](int p, int q) { return min(p, q); };
+    if (DRAFT) {
+      wave_min2(f1, f2);
+      g = wave_reduce(g, imin);
+    } else {
+      f1 = wave_reduce(f1, imin);
+    }
   }
   if (lane == 0) {
     red.zs[0][wave] = zz;
