@@ -146,6 +146,7 @@ rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
       const int64_t ncg = (M + fp.cols_per_group - 1) / fp.cols_per_group;
       items += hkv * ncg * nch;
       if (nch > 1) {
+        p.max_chunks = std::max<int32_t>(p.max_chunks, (int32_t)nch);
         // partials are stored per 32-column tile, so columns round up to 32
         part += hkv * nch * round_up(M, 32);
         comb += hkv * ((M + 31) / 32) * (L->head_dim / 32);  // 128-thread slices of a tile

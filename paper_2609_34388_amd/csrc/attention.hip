@@ -500,17 +500,21 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
 }
 
 // Merge of the split-KV partials.  Work item = (request, KV head, 32-column
-// tile, slice of 128 16-byte rows of the tile's fragment-ordered block); a
-// thread owns one row (8 head dims of one column: two runs of 4), reads that
-// row and its column's (max, sum) from every chunk -- eight chunks' loads in
-// flight at a time -- merges them with online rescaling (chunk weight
-// exp(m_c - m) * l_c on the chunk's normalised output) and writes 8 bf16
-// outputs.
-constexpr int kCombThreads = 128;
+// tile, slice of 128 16-byte rows of the tile's fragment-ordered block).  A
+// row (8 head dims of one column: two runs of 4) is merged by PARTS threads:
+// part j takes chunks j, j + PARTS, ... -- up to eight chunks' loads in
+// flight at a time -- and merges them with online rescaling (chunk weight
+// exp(m_c - m) * l_c on the chunk's normalised output); the parts' states
+// then meet in LDS and part 0 merges them in order and writes 8 bf16
+// outputs.  PARTS is 4 when some request of the launch has more than 8
+// chunks and the grid is small (up to 32 chunks then cost one memory round
+// trip on a latency-bound launch), else 1.
+constexpr int kCombRows = 128;  // 16-byte rows per work item
 
-template <int D>
-__global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnArgs a, AttnPlan p) {
-  constexpr int SLICES = 4 * D / kCombThreads;  // 16-byte rows per tile block / threads
+template <int D, int PARTS>
+__global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArgs a, AttnPlan p) {
+  constexpr int SLICES = 4 * D / kCombRows;  // 16-byte rows per tile block / rows per item
+  __shared__ float st[PARTS > 1 ? PARTS - 1 : 1][10][kCombRows];  // parts 1.. : (m, l, o[8]) per row
   const int item = xcd_item(p.grid_comb);
   if (item >= p.total_comb) return;
   const int r = find_request(p, item, true);
@@ -525,22 +529,34 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnArgs a, 
   const int tiles = M32 / 32;
   const int tile = local % tiles;
   const int hk = local / tiles;
-  const int f = slice * kCombThreads + (int)threadIdx.x;  // row of the block
+  const int t = (int)threadIdx.x % kCombRows;
+  const int part = __builtin_amdgcn_readfirstlane((int)threadIdx.x / kCombRows);
+  const int f = slice * kCombRows + t;  // row of the block
   const int lane = f & 63, lc = lane & 31, lh = lane >> 5, q = f >> 6;
   const size_t base = (size_t)rq.part_start + (size_t)hk * nch * M32 + (size_t)tile * 32;
 
   float m = kNegInf, l = 0.f;
   float o[8];
   for (int e = 0; e < 8; ++e) o[e] = 0.f;
-  for (int c0 = 0; c0 < nch; c0 += 8) {
+  auto absorb = [&](float mc, float lw, const float (&oc)[8]) {
+    const float m_new = fmaxf(m, mc);
+    const float a0 = __builtin_amdgcn_exp2f((m - m_new) * a.scale_log2);
+    const float a1 = __builtin_amdgcn_exp2f((mc - m_new) * a.scale_log2) * lw;
+    l = l * a0 + a1;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = o[e] * a0 + oc[e] * a1;
+    m = m_new;
+  };
+  for (int c0 = part; c0 < nch; c0 += 8 * PARTS) {
     float2 ml[8];
     u32x4 v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       ml[u] = make_float2(kNegInf, 0.f);
       v[u] = u32x4{0u, 0u, 0u, 0u};
-      if (c0 + u < nch) {
-        const size_t t0 = base + (size_t)(c0 + u) * M32;
+      const int c = c0 + u * PARTS;
+      if (c < nch) {
+        const size_t t0 = base + (size_t)c * M32;
         ml[u] = *(const float2*)(a.part_ml + 2 * (t0 + lc));
         v[u] = *(const u32x4*)(a.part_o + t0 * D + (size_t)f * 8);
       }
@@ -548,17 +564,38 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnArgs a, 
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       if (ml[u].x == kNegInf) continue;  // no key of that chunk is visible to this column
-      const float m_new = fmaxf(m, ml[u].x);
-      const float a0 = __builtin_amdgcn_exp2f((m - m_new) * a.scale_log2);
-      const float a1 = __builtin_amdgcn_exp2f((ml[u].x - m_new) * a.scale_log2) * ml[u].y;
-      l = l * a0 + a1;
+      float oc[8];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        o[2 * e] = o[2 * e] * a0 + __uint_as_float(v[u][e] << 16) * a1;
-        o[2 * e + 1] = o[2 * e + 1] * a0 + __uint_as_float(v[u][e] & 0xffff0000u) * a1;
+        oc[2 * e] = __uint_as_float(v[u][e] << 16);
+        oc[2 * e + 1] = __uint_as_float(v[u][e] & 0xffff0000u);
       }
-      m = m_new;
+      // the chunk's normalised output weighs in with its sum: unnormalised o_c = l_c * oc
+      absorb(ml[u].x, ml[u].y, oc);
     }
+  }
+  // Parts 1.. hand (m, l, normalised o) to part 0.
+  if (PARTS > 1 && part > 0) {
+    float* s = &st[part - 1][0][t];
+    s[0] = m;
+    s[kCombRows] = l;
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[(2 + e) * kCombRows] = o[e] * inv;
+  }
+  if (PARTS > 1) {
+    __syncthreads();
+    if (part > 0) return;
+  }
+#pragma unroll
+  for (int j = 0; j < PARTS - 1; ++j) {
+    const float* s = &st[j][0][t];
+    const float mj = s[0];
+    if (mj == kNegInf) continue;
+    float oc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) oc[e] = s[(2 + e) * kCombRows];
+    absorb(mj, s[kCombRows], oc);
   }
   const int gc = tile * 32 + lc;
   if (gc >= M) return;
@@ -583,7 +620,10 @@ hipError_t launch_impl(const AttnArgs& args, const AttnPlan& plan, hipStream_t s
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (plan.total_comb > 0) {
-    hipLaunchKernelGGL((attn_combine_kernel<D>), dim3(plan.grid_comb), dim3(kCombThreads), 0, stream, args, plan);
+    if (plan.max_chunks > 8 && plan.grid_comb <= 1024)  // long rows, and few enough items to be latency-bound
+      hipLaunchKernelGGL((attn_combine_kernel<D, 4>), dim3(plan.grid_comb), dim3(kCombRows * 4), 0, stream, args, plan);
+    else
+      hipLaunchKernelGGL((attn_combine_kernel<D, 1>), dim3(plan.grid_comb), dim3(kCombRows), 0, stream, args, plan);
     e = hipGetLastError();
   }
   return e;

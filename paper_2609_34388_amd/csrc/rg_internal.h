@@ -35,7 +35,7 @@ struct AttnPlan {
   int32_t grid_items;      // total_items rounded up to a multiple of 8
   int32_t grid_comb;       // total_comb rounded up to a multiple of 8
   int32_t cols_per_group;  // query columns one work group covers (256)
-  int32_t pad;
+  int32_t max_chunks;      // most chunks of one split request (picks the combine variant)
   AttnReq req[kMaxReqPerLaunch + 1];  // entry num_req holds the end sentinels
 };
 static_assert(sizeof(AttnPlan) <= 3700, "attention plan must fit the kernel argument block");
