@@ -139,6 +139,23 @@ def test_empty_requests_and_workspace_reuse():
         assert torch.equal(a[k], b[k]), k
 
 
+@pytest.mark.parametrize("rows,reqs", [(16, 9), (17, 9), (16, 1), (40, 300)])
+def test_finalize_group_layouts(rows, reqs):
+    """Requests of many sizes (empty ones among them, more requests than a
+    work group has threads) over a 16-chunk vocabulary give the oracle's
+    accept lengths, next tokens and e_t."""
+    vocab = 128250  # 16 chunks of 8192 entries: 16 lanes per row
+    g = torch.Generator(device=DEV).manual_seed(rows * 1000 + reqs)
+    logits = (torch.randn(rows, vocab, generator=g, device=DEV) * 2).to(torch.bfloat16)
+    cuts = np.sort(np.random.default_rng(rows + reqs).integers(0, rows + 1, size=reqs - 1))
+    rp = np.concatenate([[0], cuts, [rows]]).astype(np.int32)  # some requests empty
+    tok = torch.argmax(logits.float(), dim=1).to(torch.int32)
+    tok[rows // 2] = (tok[rows // 2] + 1) % vocab
+    res = binding.verify_accept(logits, torch.as_tensor(rp, device=DEV), tok)
+    torch.cuda.synchronize()
+    check_verify(logits, rp, tok, res)
+
+
 def test_no_verify_rows_at_all():
     rp = torch.zeros(4, dtype=torch.int32, device=DEV)
     logits = torch.empty(0, 128, dtype=torch.bfloat16, device=DEV)
