@@ -60,15 +60,18 @@ struct FullPlan {
 };
 
 // Keys per work item.  An item costs a fixed start-up and wind-down (request
-// lookup, page numbers, first copies, epilogue) besides its keys, and
-// splitting a request adds partial outputs and the combine kernel; items are
-// dispatched longest request first.  `pair_keys` holds T of every (request,
-// KV head, column group); with S = sum / 256 (one CU's share of the keys):
-//  - no split when the pairs alone give three items per CU and none exceeds
-//    S / 2 (the longest-first order then balances them);
-//  - otherwise the longest chunk (a multiple of the LDS buffer) that keeps
-//    every item within S / 4 and gives at least two items per CU, but no
-//    shorter than 256 keys.
+// lookup, page numbers, first copies, epilogue: several microseconds) besides
+// its keys, and splitting a request adds partial outputs and the combine
+// kernel; items are dispatched longest request first, so with a couple of
+// items per CU the dispatcher balances them.  `pair_keys` holds T of every
+// (request, KV head, column group); with S = sum / 256 (one CU's share): the
+// longest chunk (a multiple of the LDS buffer, at least 256 keys, at most S)
+// that still gives at least two items per CU -- no split at all when the
+// pairs alone do and none exceeds S.  Measured against the earlier rule
+// (chunks within S / 4, three pairs per CU before a request stays whole):
+// `long` 1368 -> 1340 us (whole requests), `mid` 103 -> 100 us.  Uneven
+// splits are what hurt: at `long`, 24576-key chunks (a full chunk plus a
+// short remainder per request) took 1633 us.
 int choose_chunk(const std::vector<int64_t>& pair_keys) {
   const int forced = env_int("RG_ATTN_CHUNK", 0);
   if (forced > 0) return (int)std::min<int64_t>(kMaxChunkKeys, round_up(forced, kKeyTile));
@@ -81,13 +84,12 @@ int choose_chunk(const std::vector<int64_t>& pair_keys) {
   }
   const int64_t share = total / kCUs;
   const int64_t whole = std::min<int64_t>(kMaxChunkKeys, std::max(floor_keys, round_up(longest, kKeyTile)));
-  if ((int64_t)pair_keys.size() >= 3 * kCUs && longest <= share / 2) return (int)whole;
   auto items = [&](int64_t chunk) {
     int64_t n = 0;
     for (int64_t t : pair_keys) n += (t + chunk - 1) / chunk;
     return n;
   };
-  int64_t hi = std::min(whole, std::max(floor_keys, round_up(share / 4, kKeyTile)));
+  int64_t hi = std::min(whole, std::max(floor_keys, round_up(share, kKeyTile)));
   int64_t lo = floor_keys;
   if (items(lo) < 2 * kCUs) return (int)lo;
   while (lo < hi) {  // invariant: items(lo) >= 2 * kCUs
