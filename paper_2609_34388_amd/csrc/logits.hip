@@ -39,6 +39,8 @@ constexpr int kNoIndex = 0x7fffffff;
 constexpr int kBatchRows = 1024;                       // verify rows scanned per pass
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
@@ -49,9 +51,36 @@ __device__ __forceinline__ int xcd_item(int grid_items) {
   return (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
 }
 
+// Maximum and median of loaded values through the instructions themselves:
+// fmaxf / fmed3 on values the compiler cannot prove canonical get a quieting
+// v_max_f32 x, x, x per input first (one more instruction per entry).  The
+// inputs here are finite or -inf (padding), where the two agree.
+__device__ __forceinline__ float max3_of(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ __forceinline__ float max2_of(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ float med3_of(float a, float b, float c) {
+  float r;
+  asm("v_med3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 // Vocabulary index of this thread's entry k of the chunk starting at v0.
 __device__ __forceinline__ int entry_index(int v0, int k) {
   return v0 + ((k >> 3) * kLogitThreads + (int)threadIdx.x) * 8 + (k & 7);
+}
+
+// bf16 -> fp32 of 8 packed values (two shifts per pair).
+__device__ __forceinline__ void widen8(u32x4 w, float* x) {
+  const f32x8 f = __builtin_convertvector(__builtin_bit_cast(bf16x8, w), f32x8);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) x[j] = f[j];
 }
 
 // This thread's entries of chunk [v0, v1) of `row`; entries past v1 are -inf.
@@ -63,26 +92,17 @@ __device__ __forceinline__ void load_chunk(const uint16_t* row, int v0, int v1, 
     for (int u = 0; u < kU; ++u)
       w[u] = __builtin_nontemporal_load((const u32x4*)(row + v0 + (u * kLogitThreads + tid) * 8));
 #pragma unroll
-    for (int u = 0; u < kU; ++u)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[8 * u + 2 * e] = __uint_as_float(w[u][e] << 16);
-        x[8 * u + 2 * e + 1] = __uint_as_float(w[u][e] & 0xffff0000u);
-      }
+    for (int u = 0; u < kU; ++u) widen8(w[u], x + 8 * u);
     return;
   }
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
     const int base = v0 + (u * kLogitThreads + tid) * 8;
     if (vec && base + 8 <= v1) {
-      const u32x4 t = *(const u32x4*)(row + base);
-      for (int e = 0; e < 4; ++e) {
-        x[8 * u + 2 * e] = __uint_as_float(t[e] << 16);
-        x[8 * u + 2 * e + 1] = __uint_as_float(t[e] & 0xffff0000u);
-      }
+      widen8(*(const u32x4*)(row + base), x + 8 * u);
     } else {
       for (int j = 0; j < 8; ++j)
-        x[8 * u + j] = (base + j < v1) ? __uint_as_float((uint32_t)row[base + j] << 16) : kNegInf;
+        x[8 * u + j] = (base + j < v1) ? (float)__builtin_bit_cast(__bf16, row[base + j]) : kNegInf;
     }
   }
 }
@@ -230,8 +250,8 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
       float t1 = kNegInf, t2 = kNegInf;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        t2 = __builtin_amdgcn_fmed3f(t1, t2, x[8 * u + j]);
-        t1 = fmaxf(t1, x[8 * u + j]);
+        t2 = med3_of(t1, t2, x[8 * u + j]);
+        t1 = max2_of(t1, x[8 * u + j]);
       }
       gm[u] = t1;
       g2[u] = t2;
@@ -244,11 +264,11 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
       const float* y = x + 8 * u;
-      gm[u] = fmaxf(fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])), fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7])));
+      gm[u] = max3_of(max3_of(y[0], y[1], y[2]), max3_of(y[3], y[4], y[5]), max2_of(y[6], y[7]));
     }
     a1 = gm[0];
 #pragma unroll
-    for (int u = 1; u < kU; ++u) a1 = fmaxf(a1, gm[u]);
+    for (int u = 1; u < kU; ++u) a1 = max2_of(a1, gm[u]);
   }
   const float own1 = a1;
   if (DRAFT) wave_top2(a1, a2);
