@@ -17,3 +17,10 @@ from .recguide_oracle import (  # noqa: F401
     softmax_attention,
     softmax_row,
 )
+from .branches import (  # noqa: F401
+    branch_step_mask,
+    oracle_branch_attention,
+    oracle_match_branches,
+    oracle_plan_branches,
+    request_branches,
+)
