@@ -1,7 +1,7 @@
 """GPU parity of rg_draft_verify_attention against the fp64 oracle.
 
 Tolerance (per output row and query head): max_d |gpu - oracle| <=
-1e-2 * ||oracle row||_2 (floor 1e-6), lse within 1e-3 absolute.  Inputs are
+1e-2 * ||oracle row||_2 (floor 1e-6), lse within 2e-3 absolute.  Inputs are
 the same bf16 bits on both sides; unused cache slots and pages are poisoned
 with NaN so that any out-of-range read shows up.
 """
@@ -16,7 +16,7 @@ from paper_2609_34388_amd import workloads as W
 pytestmark = pytest.mark.gpu
 DEV = torch.device("cuda")
 ATOL_ROW = 1e-2
-LSE_ATOL = 1e-3
+LSE_ATOL = 2e-3  # log1p(2^-9): bf16-rounded probabilities in the row sum
 
 
 def run(lay, inp, **kw):
