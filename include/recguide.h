@@ -17,6 +17,16 @@
  *                              (Sec. 4.1)
  *   rg_verify_and_confidence   the two logit passes above in one call
  *
+ * and, for the predictive draft-verify overlap (Sec. 5.1, served as in
+ * Sec. 5.3):
+ *
+ *   rg_multibranch_attention   the step's attention when the rows after the
+ *                              verify rows are several branches (correction
+ *                              and continuation drafts) that share the
+ *                              canonical prefix, read once for all of them
+ *   rg_plan_branches           risky positions and the branches to prepare
+ *   rg_match_branches          which prepared branch a verification confirms
+ *
  * Conventions shared by every entry point
  * ---------------------------------------
  * - bf16 tensors are passed as their raw 16-bit patterns (uint16_t).
@@ -49,7 +59,7 @@
 extern "C" {
 #endif
 
-#define RG_ABI_VERSION 1
+#define RG_ABI_VERSION 2
 
 typedef int32_t rg_status;
 #define RG_OK 0
@@ -206,6 +216,103 @@ rg_status rg_verify_and_confidence(const uint16_t* verify_logits, int64_t verify
                                    float* row_entropy, float* accept_entropy, int32_t draft_rows,
                                    int32_t* top1, int32_t* top2, float* p1, float* p2, float* margin,
                                    float* entropy, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Predictive draft-verify overlap (Sec. 5.1, Sec. 5.3)
+ * ------------------------------------------------------------------------ */
+
+/* Largest number of requests planned into one multi-branch attention launch
+ * (larger batches are split into several launches by the library). */
+#define RG_BRANCH_MAX_REQS_PER_LAUNCH 64
+
+/*
+ * Branches of each request of a step (host arrays, read during the call).
+ *
+ * Request r lists branches branch_indptr[r] .. branch_indptr[r+1]-1, at most
+ * three.  Its query rows (rg_attn_layout) are its n_verify[r] = V verify rows
+ * followed by each listed branch's rows in order, and its keys are its
+ * ctx_len[r] = L cached tokens, the V verify rows, then the branch rows in
+ * the same order (their K/V written to the request's pages like any token).
+ * A branch k keeps the canonical prefix of the context and its first
+ * prefix[k] verify rows, then has rows[k] rows of its own, the first lead[k]
+ * of which are committed tokens (e.g. a correction token) and the rest a
+ * draft block.  Mask (Eq. 1 applied to the branch's own sequence): a lead
+ * row sees the kept prefix and the branch's rows up to itself; a draft row
+ * sees the kept prefix and all of the branch's rows.  Verify row i sees keys
+ * j <= L + i as in rg_draft_verify_attention; no row sees another branch.
+ * A request listing no branch treats its rows after the verify rows as one
+ * continuation block (prefix V, lead 0): exactly rg_draft_verify_attention.
+ *
+ *   branch_indptr  host [R+1], branch_indptr[0] = 0, nondecreasing
+ *   prefix         host [branch_indptr[R]], 0 .. V (at most 4095)
+ *   lead           host [branch_indptr[R]], 0 .. rows (at most 15)
+ *   rows           host [branch_indptr[R]], >= 1 (at most 65535); the listed
+ *                  rows of a request sum to its rows after the verify rows
+ * Violations give RG_ERR_SHAPE; more than three branches or a value past
+ * its packing limit RG_ERR_UNSUPPORTED.
+ */
+typedef struct rg_branch_layout {
+  const int32_t* branch_indptr;
+  const int32_t* prefix;
+  const int32_t* lead;
+  const int32_t* rows;
+} rg_branch_layout;
+
+/* Workspace bytes rg_multibranch_attention needs (same arguments). */
+rg_status rg_multibranch_attention_workspace(const rg_attn_layout* layout,
+                                             const rg_branch_layout* branches, size_t* bytes);
+
+/*
+ * Attention of a step whose rows after the verify rows are overlap branches
+ * (Sec. 5.1) that share the canonical prefix: every key of a request,
+ * prefix included, is read from HBM once for all its rows (the shared-prefix
+ * access of Sec. 5.3), and only valid query rows are processed.  Tensors,
+ * output, lse and workspace as in rg_draft_verify_attention.
+ */
+rg_status rg_multibranch_attention(const rg_attn_layout* layout, const rg_branch_layout* branches,
+                                   const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                                   uint16_t* out, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Branches to prepare for each request's draft block (Sec. 5.1).
+ *
+ *   margin, top2   DEVICE [total_rows] draft margin P_1st - P_2nd and
+ *                  second-ranked token of each draft row (rg_draft_confidence
+ *                  outputs of the block's rows)
+ *   row_indptr     DEVICE [R+1]: request r's block is rows row_indptr[r] ..
+ *                  row_indptr[r+1]-1, at positions 0, 1, ... (at most 65535
+ *                  rows per request)
+ *   delta          positions with margin < delta are risky
+ * Outputs (DEVICE, int32): n_risky [R] risky positions in the block;
+ * n_corr [R] = min(n_risky, 2) correction branches; corr_pos [R][2] their
+ * positions (the earliest two risky ones, ascending; -1 past n_corr);
+ * corr_tok [R][2] the replacement token top2 there (-1 past n_corr);
+ * continuation [R] 1 when a continuation branch is prepared (n_risky <= 2).
+ */
+rg_status rg_plan_branches(const float* margin, const int32_t* top2, const int32_t* row_indptr,
+                           int32_t num_requests, int32_t total_rows, float delta, int32_t* n_risky,
+                           int32_t* n_corr, int32_t* corr_pos, int32_t* corr_tok, int32_t* continuation,
+                           void* stream);
+
+/*
+ * Which prepared branch each request's verification confirms (Sec. 5.1).
+ *
+ *   accept_len, next_token  DEVICE [R] rg_verify_accept outputs of the block
+ *   block_len               DEVICE [R] draft tokens of the block (full
+ *                           acceptance = accept_len == block_len, with
+ *                           next_token then the verifier's bonus token)
+ *   n_corr, corr_pos, corr_tok, continuation
+ *                           DEVICE rg_plan_branches outputs for the block
+ *   cont_first              DEVICE [R] first token of the continuation branch
+ * Output reused [R] (DEVICE int32): c when correction branch c matched
+ * (accept_len == corr_pos[r][c] and next_token == corr_tok[r][c]); n_corr[r]
+ * (the continuation's place after the corrections) when the continuation
+ * matched (full acceptance, next_token == cont_first[r]); -1 otherwise.
+ */
+rg_status rg_match_branches(const int32_t* accept_len, const int32_t* next_token, const int32_t* block_len,
+                            const int32_t* n_corr, const int32_t* corr_pos, const int32_t* corr_tok,
+                            const int32_t* continuation, const int32_t* cont_first, int32_t num_requests,
+                            int32_t* reused, void* stream);
 
 #ifdef __cplusplus
 }

@@ -42,6 +42,11 @@ class AttnLayout(ctypes.Structure):
                 ("page_indices", ctypes.c_void_p)]
 
 
+class BranchLayout(ctypes.Structure):
+    _fields_ = [("branch_indptr", ctypes.c_void_p), ("prefix", ctypes.c_void_p),
+                ("lead", ctypes.c_void_p), ("rows", ctypes.c_void_p)]
+
+
 class AttnPlanInfo(ctypes.Structure):
     _fields_ = [("num_launches", ctypes.c_int32), ("chunk_keys", ctypes.c_int32),
                 ("work_items", ctypes.c_int64), ("split_requests", ctypes.c_int64),
@@ -51,7 +56,9 @@ class AttnPlanInfo(ctypes.Structure):
 EXPORTS = ("rg_abi_version", "rg_status_string", "rg_draft_verify_attention_workspace",
            "rg_draft_verify_attention", "rg_draft_verify_attention_plan",
            "rg_verify_accept_workspace", "rg_verify_accept", "rg_draft_confidence_workspace",
-           "rg_draft_confidence", "rg_verify_and_confidence_workspace", "rg_verify_and_confidence")
+           "rg_draft_confidence", "rg_verify_and_confidence_workspace", "rg_verify_and_confidence",
+           "rg_multibranch_attention_workspace", "rg_multibranch_attention", "rg_plan_branches",
+           "rg_match_branches")
 
 _LIB = None
 
@@ -77,6 +84,12 @@ def _lib():
         "rg_verify_and_confidence_workspace": (I32, [I32, I32, I32, I32, ctypes.POINTER(SZ)]),
         "rg_verify_and_confidence": (I32, [P, I64, P, I64, I32, I32, I32, P, P, P, P, P, P, P,
                                            I32, P, P, P, P, P, P, P, SZ, P]),
+        "rg_multibranch_attention_workspace": (I32, [ctypes.POINTER(AttnLayout), ctypes.POINTER(BranchLayout),
+                                                     ctypes.POINTER(SZ)]),
+        "rg_multibranch_attention": (I32, [ctypes.POINTER(AttnLayout), ctypes.POINTER(BranchLayout),
+                                           P, P, P, P, P, P, SZ, P]),
+        "rg_plan_branches": (I32, [P, P, P, I32, I32, ctypes.c_float, P, P, P, P, P, P]),
+        "rg_match_branches": (I32, [P, P, P, P, P, P, P, P, I32, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -216,6 +229,112 @@ def draft_verify_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torc
                                           ws_bytes, _stream(stream))
     _check(st, "rg_draft_verify_attention")
     return out, lse
+
+
+class _Branches:
+    """Host arrays of the overlap branches, kept alive with the C struct."""
+
+    def __init__(self, branch_indptr, prefix, lead, rows):
+        self.branch_indptr = _host_i32(branch_indptr, "branch_indptr")
+        self.prefix = _host_i32(prefix, "prefix")
+        self.lead = _host_i32(lead, "lead")
+        self.rows = _host_i32(rows, "rows")
+        nb = int(self.branch_indptr[-1]) if self.branch_indptr.size else 0
+        for name in ("prefix", "lead", "rows"):
+            if getattr(self, name).shape[0] < nb:
+                raise ValueError(f"{name} is shorter than branch_indptr[-1]")
+        self.c = BranchLayout(self.branch_indptr.ctypes.data, self.prefix.ctypes.data,
+                              self.lead.ctypes.data, self.rows.ctypes.data)
+
+
+def make_branches(branch_indptr, prefix, lead, rows) -> _Branches:
+    return _Branches(branch_indptr, prefix, lead, rows)
+
+
+def multibranch_workspace_bytes(layout: _Layout, branches: _Branches) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib().rg_multibranch_attention_workspace(ctypes.byref(layout.c), ctypes.byref(branches.c),
+                                                     ctypes.byref(n)), "rg_multibranch_attention_workspace")
+    return int(n.value)
+
+
+def multibranch_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, layout: _Layout,
+                          branches: _Branches, *, out: Optional[torch.Tensor] = None,
+                          lse: Optional[torch.Tensor] = None, want_lse: bool = True,
+                          workspace: Optional[torch.Tensor] = None,
+                          stream=None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Attention of a step with overlap branches (rg_multibranch_attention);
+    tensors as in draft_verify_attention, the layout from make_layout and
+    the branch lists from make_branches."""
+    _dev(q, "q", torch.bfloat16)
+    _dev(k_cache, "k_cache", torch.bfloat16)
+    _dev(v_cache, "v_cache", torch.bfloat16)
+    if v_cache.shape != (k_cache.shape[0], k_cache.shape[1], k_cache.shape[3], 16):
+        raise ValueError("v_cache must be [pages, Hkv, D, 16]")
+    if int(layout.q_indptr[-1]) != q.shape[0]:
+        raise ValueError("q_indptr[-1] must equal the number of query rows")
+    if branches.branch_indptr.shape[0] != layout.ctx_len.shape[0] + 1:
+        raise ValueError("branch_indptr must have num_requests + 1 entries")
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, "out", torch.bfloat16)
+    if lse is None and want_lse:
+        lse = torch.empty(q.shape[0], q.shape[1], dtype=torch.float32, device=q.device)
+    if lse is not None:
+        _dev(lse, "lse", torch.float32)
+    need = multibranch_workspace_bytes(layout, branches)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ws_ptr = _ptr(workspace) if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st = _lib().rg_multibranch_attention(ctypes.byref(layout.c), ctypes.byref(branches.c), q.data_ptr(),
+                                         k_cache.data_ptr(), v_cache.data_ptr(), out.data_ptr(), _ptr(lse),
+                                         ws_ptr, ws_bytes, _stream(stream))
+    _check(st, "rg_multibranch_attention")
+    return out, lse
+
+
+def plan_branches(margin: torch.Tensor, top2: torch.Tensor, row_indptr: torch.Tensor, delta: float, *,
+                  out: Optional[Dict[str, torch.Tensor]] = None, stream=None) -> Dict[str, torch.Tensor]:
+    """Risky positions and branches of each request's draft block
+    (rg_plan_branches); margin fp32 / top2 int32 per draft row, row_indptr
+    int32 [R+1] on the device."""
+    _dev(margin, "margin", torch.float32)
+    _dev(top2, "top2", torch.int32)
+    _dev(row_indptr, "row_indptr", torch.int32)
+    R = row_indptr.numel() - 1
+    dev = margin.device
+    if out is None:
+        out = dict(n_risky=torch.empty(R, dtype=torch.int32, device=dev),
+                   n_corr=torch.empty(R, dtype=torch.int32, device=dev),
+                   corr_pos=torch.empty(R, 2, dtype=torch.int32, device=dev),
+                   corr_tok=torch.empty(R, 2, dtype=torch.int32, device=dev),
+                   continuation=torch.empty(R, dtype=torch.int32, device=dev))
+    st = _lib().rg_plan_branches(_ptr(margin), _ptr(top2), row_indptr.data_ptr(), R, margin.numel(),
+                                 ctypes.c_float(delta), out["n_risky"].data_ptr(), out["n_corr"].data_ptr(),
+                                 out["corr_pos"].data_ptr(), out["corr_tok"].data_ptr(),
+                                 out["continuation"].data_ptr(), _stream(stream))
+    _check(st, "rg_plan_branches")
+    return out
+
+
+def match_branches(accept_len: torch.Tensor, next_token: torch.Tensor, block_len: torch.Tensor,
+                   plan: Dict[str, torch.Tensor], cont_first: torch.Tensor, *,
+                   out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Index of the branch each request's verification confirms, or -1
+    (rg_match_branches); all int32 device tensors, `plan` from plan_branches."""
+    for name, t in (("accept_len", accept_len), ("next_token", next_token), ("block_len", block_len),
+                    ("cont_first", cont_first)):
+        _dev(t, name, torch.int32)
+    R = accept_len.numel()
+    if out is None:
+        out = torch.empty(R, dtype=torch.int32, device=accept_len.device)
+    st = _lib().rg_match_branches(accept_len.data_ptr(), next_token.data_ptr(), block_len.data_ptr(),
+                                  plan["n_corr"].data_ptr(), plan["corr_pos"].data_ptr(),
+                                  plan["corr_tok"].data_ptr(), plan["continuation"].data_ptr(),
+                                  cont_first.data_ptr(), R, out.data_ptr(), _stream(stream))
+    _check(st, "rg_match_branches")
+    return out
 
 
 def verify_accept_workspace_bytes(num_requests: int, total_rows: int, vocab: int) -> int:

@@ -50,8 +50,36 @@ rg_status validate_layout(const rg_attn_layout* L) {
   return RG_OK;
 }
 
-struct FullPlan {
-  std::vector<AttnPlan> launches;
+// Branch layout of the overlap (Sec. 5.1): at most three branches per
+// request, each within its packing limits, and a listed set of branches
+// covers exactly the request's rows after its verify rows.
+rg_status validate_branches(const rg_attn_layout* L, const rg_branch_layout* B) {
+  if (B == nullptr || !B->branch_indptr) return RG_ERR_NULL;
+  if (B->branch_indptr[0] != 0) return RG_ERR_SHAPE;
+  const int nb_all = B->branch_indptr[L->num_requests];
+  if (nb_all > 0 && (!B->prefix || !B->lead || !B->rows)) return RG_ERR_NULL;
+  for (int r = 0; r < L->num_requests; ++r) {
+    const int nb = B->branch_indptr[r + 1] - B->branch_indptr[r];
+    if (nb < 0) return RG_ERR_SHAPE;
+    if (nb > 3) return RG_ERR_UNSUPPORTED;
+    if (nb == 0) continue;
+    const int64_t n = (int64_t)L->q_indptr[r + 1] - L->q_indptr[r];
+    const int V = L->n_verify[r];
+    int64_t sum = 0;
+    for (int k = B->branch_indptr[r]; k < B->branch_indptr[r + 1]; ++k) {
+      if (B->rows[k] < 1 || B->prefix[k] < 0 || B->prefix[k] > V || B->lead[k] < 0 || B->lead[k] > B->rows[k])
+        return RG_ERR_SHAPE;
+      if (B->rows[k] > 0xffff || B->prefix[k] > 0xfff || B->lead[k] > 0xf) return RG_ERR_UNSUPPORTED;
+      sum += B->rows[k];
+    }
+    if (sum != n - V) return RG_ERR_SHAPE;
+  }
+  return RG_OK;
+}
+
+template <typename Plan>
+struct FullPlanT {
+  std::vector<Plan> launches;
   int chunk = 0;
   int cols_per_group = 256;
   int64_t items = 0, split_requests = 0, max_partial_cols = 0, total_partial_cols = 0;
@@ -101,7 +129,17 @@ int choose_chunk(const std::vector<int64_t>& pair_keys) {
   return (int)lo;
 }
 
-rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
+// Branch words of request r (see AttnReqBr); all zero when B is NULL or
+// the request lists no branch.
+void branch_words(const rg_branch_layout* B, int r, int32_t (&w)[3]) {
+  w[0] = w[1] = w[2] = 0;
+  if (B == nullptr) return;
+  for (int k = B->branch_indptr[r], j = 0; k < B->branch_indptr[r + 1]; ++k, ++j)
+    w[j] = (int32_t)((uint32_t)B->rows[k] | ((uint32_t)B->prefix[k] << 16) | ((uint32_t)B->lead[k] << 28));
+}
+
+template <typename Plan, int MaxReq>
+rg_status plan_attention(const rg_attn_layout* L, const rg_branch_layout* B, FullPlanT<Plan>& fp) {
   const int R = L->num_requests;
   const int g = L->num_q_heads / L->num_kv_heads;
   const int hkv = L->num_kv_heads;
@@ -122,9 +160,9 @@ rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
     return (int64_t)L->ctx_len[x] + (L->q_indptr[x + 1] - L->q_indptr[x]) >
            (int64_t)L->ctx_len[y] + (L->q_indptr[y + 1] - L->q_indptr[y]);
   });
-  for (int r0 = 0; r0 < R; r0 += kMaxReqPerLaunch) {
-    const int cnt = std::min(kMaxReqPerLaunch, R - r0);
-    AttnPlan p;
+  for (int r0 = 0; r0 < R; r0 += MaxReq) {
+    const int cnt = std::min(MaxReq, R - r0);
+    Plan p;
     std::memset(&p, 0, sizeof(p));
     p.num_req = cnt;
     p.chunk = fp.chunk;
@@ -133,7 +171,8 @@ rg_status plan_attention(const rg_attn_layout* L, FullPlan& fp) {
     for (int k = 0; k < cnt; ++k) {
       const int r = order[r0 + k];
       const int64_t n = L->q_indptr[r + 1] - L->q_indptr[r];
-      AttnReq& q = p.req[k];
+      auto& q = p.req[k];
+      if constexpr (__is_same(Plan, AttnPlanBr)) branch_words(B, r, q.br);
       q.q_start = L->q_indptr[r];
       q.ctx = L->ctx_len[r];
       q.nv = (int32_t)(n | ((int64_t)L->n_verify[r] << 16));
@@ -201,46 +240,30 @@ const char* rg_status_string(rg_status s) {
   }
 }
 
-rg_status rg_draft_verify_attention_workspace(const rg_attn_layout* layout, size_t* bytes) {
-  if (bytes == nullptr) return RG_ERR_NULL;
-  rg_status st = validate_layout(layout);
+}  // extern "C"
+
+namespace {
+
+using FullPlan = FullPlanT<AttnPlan>;
+using FullPlanBr = FullPlanT<AttnPlanBr>;
+
+rg_status plan_plain(const rg_attn_layout* layout, FullPlan& fp) {
+  return plan_attention<AttnPlan, kMaxReqPerLaunch>(layout, nullptr, fp);
+}
+rg_status plan_branched(const rg_attn_layout* layout, const rg_branch_layout* branches, FullPlanBr& fp) {
+  rg_status st = validate_branches(layout, branches);
   if (st != RG_OK) return st;
-  FullPlan fp;
-  st = plan_attention(layout, fp);
-  if (st != RG_OK) return st;
-  *bytes = fp.ws_bytes;
-  return RG_OK;
+  return plan_attention<AttnPlanBr, kMaxReqPerLaunchBr>(layout, branches, fp);
 }
 
-rg_status rg_draft_verify_attention_plan(const rg_attn_layout* layout, rg_attn_plan_info* info) {
-  if (info == nullptr) return RG_ERR_NULL;
-  rg_status st = validate_layout(layout);
-  if (st != RG_OK) return st;
-  FullPlan fp;
-  st = plan_attention(layout, fp);
-  if (st != RG_OK) return st;
-  info->num_launches = (int32_t)fp.launches.size();
-  info->chunk_keys = fp.chunk;
-  info->work_items = fp.items;
-  info->split_requests = fp.split_requests;
-  info->partial_columns = fp.total_partial_cols;
-  info->workspace_bytes = (int64_t)fp.ws_bytes;
-  return RG_OK;
-}
-
-rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t* q,
-                                    const uint16_t* k_cache, const uint16_t* v_cache,
-                                    uint16_t* out, float* lse, void* ws, size_t ws_bytes,
-                                    void* stream) {
-  rg_status st = validate_layout(layout);
-  if (st != RG_OK) return st;
+template <typename Plan>
+rg_status run_attention(const rg_attn_layout* layout, const FullPlanT<Plan>& fp, const uint16_t* q,
+                        const uint16_t* k_cache, const uint16_t* v_cache, uint16_t* out, float* lse,
+                        void* ws, size_t ws_bytes, void* stream) {
   if (!q || !k_cache || !v_cache || !out) return RG_ERR_NULL;
   if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
       (lse && !aligned(lse, 4)) || !aligned(layout->page_indices, 4))
     return RG_ERR_UNSUPPORTED;
-  FullPlan fp;
-  st = plan_attention(layout, fp);
-  if (st != RG_OK) return st;
   if (fp.ws_bytes > 0 && (ws == nullptr || ws_bytes < fp.ws_bytes || !aligned(ws, 16))) return RG_ERR_WORKSPACE;
 
   AttnArgs a;
@@ -259,11 +282,77 @@ rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t
   a.scale_log2 = a.sm_scale * 1.4426950408889634f;
   a.rescale_gap = 8.0f / a.scale_log2;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  for (const AttnPlan& p : fp.launches) {
+  for (const Plan& p : fp.launches) {
     if (p.total_items == 0) continue;
     if (launch_attention(a, p, layout->head_dim, s) != hipSuccess) return RG_ERR_HIP;
   }
   return RG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rg_status rg_draft_verify_attention_workspace(const rg_attn_layout* layout, size_t* bytes) {
+  if (bytes == nullptr) return RG_ERR_NULL;
+  rg_status st = validate_layout(layout);
+  if (st != RG_OK) return st;
+  FullPlan fp;
+  st = plan_plain(layout, fp);
+  if (st != RG_OK) return st;
+  *bytes = fp.ws_bytes;
+  return RG_OK;
+}
+
+rg_status rg_draft_verify_attention_plan(const rg_attn_layout* layout, rg_attn_plan_info* info) {
+  if (info == nullptr) return RG_ERR_NULL;
+  rg_status st = validate_layout(layout);
+  if (st != RG_OK) return st;
+  FullPlan fp;
+  st = plan_plain(layout, fp);
+  if (st != RG_OK) return st;
+  info->num_launches = (int32_t)fp.launches.size();
+  info->chunk_keys = fp.chunk;
+  info->work_items = fp.items;
+  info->split_requests = fp.split_requests;
+  info->partial_columns = fp.total_partial_cols;
+  info->workspace_bytes = (int64_t)fp.ws_bytes;
+  return RG_OK;
+}
+
+rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t* q,
+                                    const uint16_t* k_cache, const uint16_t* v_cache,
+                                    uint16_t* out, float* lse, void* ws, size_t ws_bytes,
+                                    void* stream) {
+  rg_status st = validate_layout(layout);
+  if (st != RG_OK) return st;
+  FullPlan fp;
+  st = plan_plain(layout, fp);
+  if (st != RG_OK) return st;
+  return run_attention(layout, fp, q, k_cache, v_cache, out, lse, ws, ws_bytes, stream);
+}
+
+rg_status rg_multibranch_attention_workspace(const rg_attn_layout* layout, const rg_branch_layout* branches,
+                                             size_t* bytes) {
+  if (bytes == nullptr) return RG_ERR_NULL;
+  rg_status st = validate_layout(layout);
+  if (st != RG_OK) return st;
+  FullPlanBr fp;
+  st = plan_branched(layout, branches, fp);
+  if (st != RG_OK) return st;
+  *bytes = fp.ws_bytes;
+  return RG_OK;
+}
+
+rg_status rg_multibranch_attention(const rg_attn_layout* layout, const rg_branch_layout* branches,
+                                   const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                                   uint16_t* out, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  rg_status st = validate_layout(layout);
+  if (st != RG_OK) return st;
+  FullPlanBr fp;
+  st = plan_branched(layout, branches, fp);
+  if (st != RG_OK) return st;
+  return run_attention(layout, fp, q, k_cache, v_cache, out, lse, ws, ws_bytes, stream);
 }
 
 rg_status rg_verify_accept_workspace(int32_t num_requests, int32_t total_rows, int32_t vocab, size_t* bytes) {
@@ -405,6 +494,50 @@ rg_status rg_verify_and_confidence(const uint16_t* verify_logits, int64_t verify
                        dbytes ? w + vbytes : nullptr, dbytes, d);
   if (st != RG_OK) return st;
   return launch_round(v, d, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
+
+
+rg_status rg_plan_branches(const float* margin, const int32_t* top2, const int32_t* row_indptr,
+                           int32_t num_requests, int32_t total_rows, float delta, int32_t* n_risky,
+                           int32_t* n_corr, int32_t* corr_pos, int32_t* corr_tok, int32_t* continuation,
+                           void* stream) {
+  if (num_requests < 1 || total_rows < 0) return RG_ERR_SHAPE;
+  if (!row_indptr || !n_risky || !n_corr || !corr_pos || !corr_tok || !continuation) return RG_ERR_NULL;
+  if (total_rows > 0 && (!margin || !top2)) return RG_ERR_NULL;
+  PlanBranchArgs a;
+  a.margin = margin;
+  a.top2 = top2;
+  a.row_indptr = row_indptr;
+  a.num_req = num_requests;
+  a.delta = delta;
+  a.n_risky = n_risky;
+  a.n_corr = n_corr;
+  a.corr_pos = corr_pos;
+  a.corr_tok = corr_tok;
+  a.continuation = continuation;
+  return launch_plan_branches(a, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
+
+rg_status rg_match_branches(const int32_t* accept_len, const int32_t* next_token, const int32_t* block_len,
+                            const int32_t* n_corr, const int32_t* corr_pos, const int32_t* corr_tok,
+                            const int32_t* continuation, const int32_t* cont_first, int32_t num_requests,
+                            int32_t* reused, void* stream) {
+  if (num_requests < 1) return RG_ERR_SHAPE;
+  if (!accept_len || !next_token || !block_len || !n_corr || !corr_pos || !corr_tok || !continuation ||
+      !cont_first || !reused)
+    return RG_ERR_NULL;
+  MatchBranchArgs a;
+  a.accept_len = accept_len;
+  a.next_token = next_token;
+  a.block_len = block_len;
+  a.n_corr = n_corr;
+  a.corr_pos = corr_pos;
+  a.corr_tok = corr_tok;
+  a.continuation = continuation;
+  a.cont_first = cont_first;
+  a.num_req = num_requests;
+  a.reused = reused;
+  return launch_match_branches(a, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
 }
 
 }  // extern "C"

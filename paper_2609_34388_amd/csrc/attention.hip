@@ -64,7 +64,8 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 // Request owning work item `item`: the last r with start(r) <= item (starts
 // are nondecreasing, empty requests share their successor's start).  Every
 // lane tests one request, so the search is one round of loads, not a chain.
-__device__ __forceinline__ int find_request(const AttnPlan& p, int item, bool combine) {
+template <typename Plan>
+__device__ __forceinline__ int find_request(const Plan& p, int item, bool combine) {
   const int lane = threadIdx.x & 63;
   int r = 0;
   for (int base = 1; base < p.num_req; base += 64) {
@@ -137,8 +138,9 @@ static_assert(kSuper % kKeyTile == 0, "a super-tile is a whole number of key til
 // accepts a 1 KiB LDS-DMA instruction only every few dozen cycles, and a
 // compute wave issuing its share would stall for most of a buffer's worth of
 // them instead of computing.
-template <int D>
-__global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan p) {
+template <int D, typename Plan>
+__global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, Plan p) {
+  constexpr bool BR = __is_same(Plan, AttnPlanBr);  // rows after the verify rows form branches
   constexpr int NCH = D / 8;                   // 16-byte chunks per K row
   constexpr int KSTEPS = D / 16;               // MFMA k-steps of q.k
   constexpr int DT = D / 32;                   // 32-wide head-dim tiles of the output
@@ -165,7 +167,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   const int item = p.num_req == 1 ? xcd_item(p.grid_items) : (int)blockIdx.x;
   if (item >= p.total_items) return;
   const int r = find_request(p, item, false);
-  const AttnReq rq = p.req[r];
+  const auto rq = p.req[r];
   const int n = rq.nv & 0xffff, nver = rq.nv >> 16, L = rq.ctx, T = L + n;
   const int g = a.g;
   const int M = n * g;
@@ -219,7 +221,40 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
   const bool valid = tile_on && col < M;
   const int tok = valid ? col / g : 0;
   const int hh = col - tok * g;
-  const int lim = valid ? min(kend, tok < nver ? L + tok + 1 : T) : 0;
+  // Keys a column sees: those below lim, and with overlap branches also its
+  // branch's own rows slo .. shi - 1 (Eq. 1 on the branch's sequence: the
+  // kept canonical prefix, then the branch's committed lead rows causally,
+  // then its draft rows seeing the whole branch).  Both clipped to the chunk.
+  int lim, slo = 0, shi = 0;
+  if (!valid) {
+    lim = 0;
+  } else if (!BR || tok < nver) {
+    lim = min(kend, tok < nver ? L + tok + 1 : T);
+  } else {
+    int t = tok - nver, start = L + nver, prefix = nver, lead = 0, rows = n - nver;
+    if constexpr (BR) {
+      bool found = false;
+#pragma unroll
+      for (int bb = 0; bb < 3; ++bb) {
+        const int w = rq.br[bb];
+        const int rb = w & 0xffff;
+        if (w != 0 && !found) {
+          if (t < rb) {
+            prefix = (w >> 16) & 0xfff;
+            lead = (int)((uint32_t)w >> 28);
+            rows = rb;
+            found = true;
+          } else {
+            t -= rb;
+            start += rb;
+          }
+        }
+      }
+    }
+    lim = min(kend, L + prefix);
+    slo = start;
+    shi = min(kend, start + (t < lead ? t + 1 : rows));
+  }
   bf16x8 qf[KSTEPS];
   {
     const uint16_t* qrow = a.q + ((size_t)(rq.q_start + tok) * a.hq + hk * g + hh) * D;
@@ -314,7 +349,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int key = kbase + 16 * (i >> 3) + 8 * lh + 4 * ((i >> 2) & 1) + (i & 3);
-        if (key >= lim) sc[i] = kNegInf;
+        if (key >= lim && (!BR || (uint32_t)(key - slo) >= (uint32_t)(shi - slo))) sc[i] = kNegInf;
       }
     }
     float mx = sc[0];
@@ -511,14 +546,14 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, AttnPlan
 // trip on a latency-bound launch), else 1.
 constexpr int kCombRows = 128;  // 16-byte rows per work item
 
-template <int D, int PARTS>
-__global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArgs a, AttnPlan p) {
+template <int D, int PARTS, typename Plan>
+__global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArgs a, Plan p) {
   constexpr int SLICES = 4 * D / kCombRows;  // 16-byte rows per tile block / rows per item
   __shared__ float st[PARTS > 1 ? PARTS - 1 : 1][10][kCombRows];  // parts 1.. : (m, l, o[8]) per row
   const int item = xcd_item(p.grid_comb);
   if (item >= p.total_comb) return;
   const int r = find_request(p, item, true);
-  const AttnReq rq = p.req[r];
+  const auto rq = p.req[r];
   const int n = rq.nv & 0xffff, L = rq.ctx, T = L + n;
   const int g = a.g;
   const int M = n * g, M32 = (M + 31) & ~31;
@@ -614,16 +649,16 @@ __global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArg
   if (a.lse != nullptr && f < 32) a.lse[orow] = m * a.sm_scale + __logf(l);
 }
 
-template <int D>
-hipError_t launch_impl(const AttnArgs& args, const AttnPlan& plan, hipStream_t stream) {
-  hipLaunchKernelGGL((attn_fwd_kernel<D>), dim3(plan.grid_items), dim3(kThreads), 0, stream, args, plan);
+template <int D, typename Plan>
+hipError_t launch_impl(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
+  hipLaunchKernelGGL((attn_fwd_kernel<D, Plan>), dim3(plan.grid_items), dim3(kThreads), 0, stream, args, plan);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (plan.total_comb > 0) {
     if (plan.max_chunks > 8 && plan.grid_comb <= 1024)  // long rows, and few enough items to be latency-bound
-      hipLaunchKernelGGL((attn_combine_kernel<D, 4>), dim3(plan.grid_comb), dim3(kCombRows * 4), 0, stream, args, plan);
+      hipLaunchKernelGGL((attn_combine_kernel<D, 4, Plan>), dim3(plan.grid_comb), dim3(kCombRows * 4), 0, stream, args, plan);
     else
-      hipLaunchKernelGGL((attn_combine_kernel<D, 1>), dim3(plan.grid_comb), dim3(kCombRows), 0, stream, args, plan);
+      hipLaunchKernelGGL((attn_combine_kernel<D, 1, Plan>), dim3(plan.grid_comb), dim3(kCombRows), 0, stream, args, plan);
     e = hipGetLastError();
   }
   return e;
@@ -632,6 +667,12 @@ hipError_t launch_impl(const AttnArgs& args, const AttnPlan& plan, hipStream_t s
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& args, const AttnPlan& plan, int head_dim,
+                            hipStream_t stream) {
+  if (head_dim == 128) return launch_impl<128>(args, plan, stream);
+  return launch_impl<64>(args, plan, stream);
+}
+
+hipError_t launch_attention(const AttnArgs& args, const AttnPlanBr& plan, int head_dim,
                             hipStream_t stream) {
   if (head_dim == 128) return launch_impl<128>(args, plan, stream);
   return launch_impl<64>(args, plan, stream);

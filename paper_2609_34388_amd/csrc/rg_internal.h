@@ -27,7 +27,18 @@ struct AttnReq {
   int32_t comb_start;  // first combine work item (split requests)
 };
 
-struct AttnPlan {
+// A request of a launch with overlap branches: its rows after the verify
+// rows are up to three branches, each packed as rows (bits 0-15) | prefix
+// verify rows kept (bits 16-27) | committed lead rows (bits 28-31); br[0] = 0
+// means no branch list (the rows after the verify rows are one
+// continuation block that keeps every verify row).
+struct AttnReqBr : AttnReq {
+  int32_t br[3];
+};
+constexpr int kMaxReqPerLaunchBr = 64;  // equals RG_BRANCH_MAX_REQS_PER_LAUNCH
+
+template <typename Req, int MaxReq>
+struct AttnPlanT {
   int32_t num_req;         // requests in this launch
   int32_t chunk;           // keys per work item, multiple of kKeyTile
   int32_t total_items;     // main-kernel work items
@@ -36,9 +47,12 @@ struct AttnPlan {
   int32_t grid_comb;       // total_comb rounded up to a multiple of 8
   int32_t cols_per_group;  // query columns one work group covers (256)
   int32_t max_chunks;      // most chunks of one split request (picks the combine variant)
-  AttnReq req[kMaxReqPerLaunch + 1];  // entry num_req holds the end sentinels
+  Req req[MaxReq + 1];     // entry num_req holds the end sentinels
 };
+using AttnPlan = AttnPlanT<AttnReq, kMaxReqPerLaunch>;
+using AttnPlanBr = AttnPlanT<AttnReqBr, kMaxReqPerLaunchBr>;
 static_assert(sizeof(AttnPlan) <= 3700, "attention plan must fit the kernel argument block");
+static_assert(sizeof(AttnPlanBr) <= 3700, "attention plan must fit the kernel argument block");
 
 struct AttnArgs {
   const uint16_t* q;
@@ -57,6 +71,8 @@ struct AttnArgs {
 
 // Attention launchers (attention.hip).  `plan` is one launch's plan.
 hipError_t launch_attention(const AttnArgs& args, const AttnPlan& plan, int head_dim,
+                            hipStream_t stream);
+hipError_t launch_attention(const AttnArgs& args, const AttnPlanBr& plan, int head_dim,
                             hipStream_t stream);
 
 // Logit-row reductions (logits.hip).
@@ -102,5 +118,33 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream);
 hipError_t launch_draft(const DraftArgs& a, hipStream_t stream);
 // Verify and draft passes of one round together: two launches in all.
 hipError_t launch_round(const VerifyArgs& v, const DraftArgs& d, hipStream_t stream);
+
+// Branch planning and matching (branches.hip).
+struct PlanBranchArgs {
+  const float* margin;
+  const int32_t* top2;
+  const int32_t* row_indptr;
+  int32_t num_req;
+  float delta;
+  int32_t* n_risky;
+  int32_t* n_corr;
+  int32_t* corr_pos;
+  int32_t* corr_tok;
+  int32_t* continuation;
+};
+struct MatchBranchArgs {
+  const int32_t* accept_len;
+  const int32_t* next_token;
+  const int32_t* block_len;
+  const int32_t* n_corr;
+  const int32_t* corr_pos;
+  const int32_t* corr_tok;
+  const int32_t* continuation;
+  const int32_t* cont_first;
+  int32_t num_req;
+  int32_t* reused;
+};
+hipError_t launch_plan_branches(const PlanBranchArgs& a, hipStream_t stream);
+hipError_t launch_match_branches(const MatchBranchArgs& a, hipStream_t stream);
 
 }  // namespace rg

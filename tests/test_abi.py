@@ -87,6 +87,51 @@ def test_attention_validation_errors():
     assert _attn(_L(), q=ctypes.c_void_p(0x1002)) == 3
 
 
+def _br(indptr, prefix, lead, rows):
+    return binding.make_branches(indptr, prefix, lead, rows)
+
+
+def _mb_ws(l, b):
+    n = ctypes.c_size_t(123)
+    st = binding.library().rg_multibranch_attention_workspace(ctypes.byref(l.c), ctypes.byref(b.c), ctypes.byref(n))
+    return st, n.value
+
+
+def test_multibranch_validation_errors():
+    lib = binding.library()
+    # request 0: V = 3, 4 rows after them; request 1: V = 0, 5 rows
+    l = _L(nv=(3, 0), n=(7, 5))
+    ok = _br([0, 2, 3], [1, 3, 0], [1, 0, 0], [2, 2, 5])
+    st, n = _mb_ws(l, ok)
+    assert st == 0 and n == 0                                    # nothing is split here
+    assert _mb_ws(l, _br([0, 0, 0], [], [], []))[0] == 0         # no branches: the fused step
+    assert _mb_ws(l, _br([0, 2, 3], [1, 3, 0], [1, 0, 0], [2, 3, 5]))[0] == 2   # rows sum to 5, not 4
+    assert _mb_ws(l, _br([0, 2, 3], [4, 3, 0], [1, 0, 0], [2, 2, 5]))[0] == 2   # prefix past V
+    assert _mb_ws(l, _br([0, 2, 3], [1, 3, 0], [3, 0, 0], [2, 2, 5]))[0] == 2   # lead past rows
+    assert _mb_ws(l, _br([0, 2, 3], [1, 3, 0], [1, 0, 0], [0, 4, 5]))[0] == 2   # empty branch
+    assert _mb_ws(l, _br([1, 2, 3], [1, 3, 0], [1, 0, 0], [2, 2, 5]))[0] == 2   # branch_indptr[0] != 0
+    four = _br([0, 4, 5], [0, 1, 2, 3, 0], [0, 0, 0, 0, 0], [1, 1, 1, 1, 5])
+    assert _mb_ws(l, four)[0] == 3                               # at most three branches
+    big = _L(R=1, nv=(4100,), n=(4101,), ctx=(0,))
+    assert _mb_ws(big, _br([0, 1], [4100], [0], [1]))[0] == 3    # prefix past its 12-bit field
+    assert lib.rg_multibranch_attention_workspace(ctypes.byref(l.c), None, ctypes.byref(ctypes.c_size_t())) == 1
+    # the attention call itself validates the same way before anything runs
+    assert lib.rg_multibranch_attention(ctypes.byref(l.c), ctypes.byref(four.c), FAKE_DEV, FAKE_DEV, FAKE_DEV,
+                                        FAKE_DEV, None, None, 0, None) == 3
+    assert lib.rg_multibranch_attention(ctypes.byref(l.c), ctypes.byref(ok.c), None, FAKE_DEV, FAKE_DEV,
+                                        FAKE_DEV, None, None, 0, None) == 1
+
+
+def test_branch_plan_and_match_validation_errors():
+    lib = binding.library()
+    d = FAKE_DEV
+    assert lib.rg_plan_branches(d, d, d, 0, 4, ctypes.c_float(0.5), d, d, d, d, d, None) == 2
+    assert lib.rg_plan_branches(d, d, None, 2, 4, ctypes.c_float(0.5), d, d, d, d, d, None) == 1
+    assert lib.rg_plan_branches(None, d, d, 2, 4, ctypes.c_float(0.5), d, d, d, d, d, None) == 1
+    assert lib.rg_match_branches(d, d, d, d, d, d, d, d, 0, d, None) == 2
+    assert lib.rg_match_branches(d, d, d, d, d, d, d, None, 2, d, None) == 1
+
+
 def test_logit_validation_errors():
     lib = binding.library()
     ws = ctypes.c_void_p(0x2000)
