@@ -253,7 +253,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, Plan p) 
     }
     lim = min(kend, L + prefix);
     slo = start;
-    shi = min(kend, start + (t < lead ? t + 1 : rows));
+    // empty (shi = slo) when the chunk ends before the branch's rows begin
+    shi = max(slo, min(kend, start + (t < lead ? t + 1 : rows)));
   }
   bf16x8 qf[KSTEPS];
   {

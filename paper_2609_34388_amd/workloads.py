@@ -201,6 +201,118 @@ def make_layout(spec, seed: int = 0, *, num_requests: Optional[int] = None,
                   draft_row_indptr=_prefix(n_draft))
 
 
+
+def overlap_branches(layout: Layout):
+    """Branches of an overlap round for each request of ``layout``, in the
+    largest form Sec. 5.1 prepares: correction branches at two distinct
+    seeded positions of the V-token block under verification (one when
+    V = 1, none when V = 0), each a committed replacement token followed by a
+    B-token draft block -- (prefix = position, lead = 1, rows = 1 + B) --
+    then a continuation branch that keeps the whole block and drafts B rows
+    -- (V, 0, B).  B is the request's draft block size in ``layout``.
+    Returns one list of (prefix, lead, rows) per request."""
+    rng = np.random.default_rng(_seed_sequence(layout.spec, layout.seed).spawn(8)[6])
+    out = []
+    for r in range(layout.num_requests):
+        V, B = int(layout.n_verify[r]), int(layout.n_draft[r])
+        pos = sorted(int(p) for p in rng.choice(V, size=min(2, V), replace=False)) if V else []
+        br = [(p, 1, 1 + B) for p in pos]
+        if B:
+            br.append((V, 0, B))
+        out.append(br)
+    return out
+
+
+def _paged(layout: Layout, ctx_len, n_verify, n_draft, page_indptr, page_indices, num_pages) -> Layout:
+    z = np.zeros(len(ctx_len), dtype=np.int32)
+    ctx_len, n_verify, n_draft = (np.asarray(a, dtype=np.int32) for a in (ctx_len, n_verify, n_draft))
+    return Layout(spec=layout.spec, seed=layout.seed, ctx_len=ctx_len, n_verify=n_verify, n_draft=n_draft,
+                  sigma=np.ones(len(ctx_len)), bonus=z, q_indptr=_prefix(n_verify + n_draft),
+                  page_indptr=np.asarray(page_indptr, dtype=np.int32),
+                  page_indices=np.asarray(page_indices, dtype=np.int32), num_pages=int(num_pages),
+                  row_indptr=_prefix(n_verify), draft_row_indptr=_prefix(n_draft))
+
+
+def make_overlap_layout(layout: Layout, branches, spare_pages: int = 8) -> Layout:
+    """``layout`` with each request's rows after its verify rows replaced by
+    its branches' rows (their keys follow the verify rows in the request's
+    pages, in branch order); pages freshly permuted."""
+    rng = np.random.default_rng(_seed_sequence(layout.spec, layout.seed).spawn(8)[7])
+    n_draft = np.array([sum(b[2] for b in br) for br in branches], dtype=np.int32)
+    kv = layout.ctx_len + layout.n_verify + n_draft
+    pages = (kv + PAGE_SIZE - 1) // PAGE_SIZE
+    used = int(pages.sum())
+    order = rng.permutation(used + spare_pages)
+    return _paged(layout, layout.ctx_len, layout.n_verify, n_draft, _prefix(pages), order[:used],
+                  used + spare_pages)
+
+
+def make_separate_layout(overlap: Layout, branches) -> Tuple[Layout, list]:
+    """The same rows served without a shared prefix: every request of
+    ``overlap`` becomes one request of its verify rows plus one request per
+    branch, whose context is the branch's kept prefix (its full pages alias
+    the shared request's pages, as prefix caching would) followed by the
+    branch's own rows on fresh pages.  Returns the layout and, per new
+    request, (original request, branch index or -1)."""
+    ctx, nv, nd, counts, idx, origin = [], [], [], [], [], []
+    fresh = overlap.num_pages
+    for r, br in enumerate(branches):
+        L, V = int(overlap.ctx_len[r]), int(overlap.n_verify[r])
+        own = overlap.page_indices[int(overlap.page_indptr[r]):int(overlap.page_indptr[r + 1])]
+        if V:
+            n_pages = (L + V + PAGE_SIZE - 1) // PAGE_SIZE
+            ctx.append(L); nv.append(V); nd.append(0); counts.append(n_pages)
+            idx.extend(own[:n_pages]); origin.append((r, -1))
+        for b, (prefix, lead, rows) in enumerate(br):
+            kept = L + prefix
+            full = kept // PAGE_SIZE
+            total = (kept + rows + PAGE_SIZE - 1) // PAGE_SIZE
+            ctx.append(kept); nv.append(lead); nd.append(rows - lead); counts.append(total)
+            idx.extend(own[:full])
+            idx.extend(range(fresh, fresh + total - full))
+            fresh += total - full
+            origin.append((r, b))
+    return _paged(overlap, ctx, nv, nd, _prefix(np.asarray(counts, dtype=np.int64)), idx, fresh), origin
+
+
+def make_separate_kv(overlap: Layout, branches, separate: Layout, origin, k_cache: torch.Tensor,
+                     v_cache: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor]:
+    """K/V pools for ``make_separate_layout``'s layout holding the same keys:
+    the shared pages as they are, and on each branch request's fresh pages
+    the rest of its kept prefix and its own rows, copied from ``overlap``'s
+    pools (a data copy only)."""
+    dst_p, dst_s, src_p, src_s = [], [], [], []
+    offsets = []
+    for br in branches:
+        off, acc = [], 0
+        for b in br:
+            off.append(acc)
+            acc += b[2]
+        offsets.append(off)
+    for i, (r, b) in enumerate(origin):
+        if b < 0:
+            continue
+        L, V = int(overlap.ctx_len[r]), int(overlap.n_verify[r])
+        prefix, _, rows = branches[r][b]
+        kept = L + prefix
+        first = (kept // PAGE_SIZE) * PAGE_SIZE
+        j = np.arange(first, kept + rows)
+        src = np.where(j < kept, j, L + V + offsets[r][b] + (j - kept))
+        own = overlap.page_indices[int(overlap.page_indptr[r]):]
+        sp = separate.page_indices[int(separate.page_indptr[i]):]
+        dst_p.append(sp[j // PAGE_SIZE]); dst_s.append(j % PAGE_SIZE)
+        src_p.append(own[src // PAGE_SIZE]); src_s.append(src % PAGE_SIZE)
+    k = torch.zeros((separate.num_pages,) + tuple(k_cache.shape[1:]), dtype=k_cache.dtype, device=k_cache.device)
+    v = torch.zeros((separate.num_pages,) + tuple(v_cache.shape[1:]), dtype=v_cache.dtype, device=v_cache.device)
+    k[:k_cache.shape[0]] = k_cache
+    v[:v_cache.shape[0]] = v_cache
+    if dst_p:
+        t = lambda a: torch.as_tensor(np.concatenate(a).astype(np.int64), device=k_cache.device)
+        dp, ds, sp_, ss = t(dst_p), t(dst_s), t(src_p), t(src_s)
+        k[dp, :, ds, :] = k_cache[sp_, :, ss, :]
+        v[dp, :, :, ds] = v_cache[sp_, :, :, ss]
+    return k, v
+
 def _gen(layout: Layout, device, stream: int) -> torch.Generator:
     ss = _seed_sequence(layout.spec, layout.seed).spawn(8)[stream]
     g = torch.Generator(device=device)

@@ -88,6 +88,9 @@ CASES = {
     "split": ([2500, 1300], [16, 4], [[(3, 1, 16), (9, 1, 16), (16, 0, 16)], [(4, 0, 9)]]),
     # many columns: 64 rows = 256 columns of one KV head (8 tiles)
     "wide": ([700], [16], [[(5, 1, 16), (11, 1, 16), (16, 0, 16)]]),
+    # chunk boundaries between a branch's kept prefix and its own rows (the
+    # first branch spans more keys than any chunk)
+    "gap": ([3000, 700], [4, 2], [[(0, 0, 600), (1, 1, 5), (4, 0, 7)], [(0, 1, 300), (2, 0, 3)]]),
 }
 
 
@@ -190,3 +193,38 @@ def test_plan_and_match_branches_match_oracle(seed):
                                           want["continuation"], cont_first)
     np.testing.assert_array_equal(reused.cpu().numpy(), want_r)
     assert (want_r >= 0).sum() > R // 10  # the outcomes above do hit branches
+
+
+@pytest.mark.parametrize("workload", ["mid", "high"])
+def test_overlap_round_full_size(workload):
+    """A full-size overlap round (every request with two correction branches
+    and a continuation, the layout the benchmark times): sampled requests
+    against the oracle, and every row against the same rows served as
+    separate requests (each branch with its own copy of the kept prefix)
+    through rg_draft_verify_attention."""
+    lay = W.make_layout(workload, seed=4)
+    branches = W.overlap_branches(lay)
+    ov = W.make_overlap_layout(lay, branches)
+    inp = W.make_attention_inputs(ov, DEV, poison=float("nan"))
+    out, lse = _run(ov, inp, branches)
+    rng = np.random.default_rng(4)
+    reqs = sorted(rng.choice(ov.num_requests, size=min(3, ov.num_requests), replace=False).tolist())
+    heads = [0, 13, 31]
+    ref = oracle.oracle_branch_attention(W.bf16_bits(inp["q"]), W.bf16_bits(inp["k_cache"]),
+                                         W.bf16_bits(inp["v_cache"]), ov.q_indptr, ov.n_verify, ov.ctx_len,
+                                         ov.page_indptr, ov.page_indices, branches, requests=reqs, heads=heads)
+    for r in reqs:
+        q0, q1 = int(ov.q_indptr[r]), int(ov.q_indptr[r + 1])
+        for h in heads:
+            _check(out[q0:q1, h:h + 1], lse[q0:q1, h:h + 1],
+                   dict(out=ref["out"][q0:q1, h:h + 1], lse=ref["lse"][q0:q1, h:h + 1]))
+    sep, origin = W.make_separate_layout(ov, branches)
+    k2, v2 = W.make_separate_kv(ov, branches, sep, origin, inp["k_cache"], inp["v_cache"])
+    sidx = torch.as_tensor(sep.page_indices, device=DEV)
+    out_s, lse_s = binding.draft_verify_attention(inp["q"], k2, v2, sep.q_indptr, sep.n_verify, sep.ctx_len,
+                                                  sep.page_indptr, sidx)
+    torch.cuda.synchronize()
+    a, b = out.double(), out_s.double()
+    err = ((a - b).abs().amax(-1) / b.norm(dim=-1).clamp_min(1e-6)).max().item()
+    assert err <= 2 * ATOL_ROW
+    assert (lse.double() - lse_s.double()).abs().max().item() <= 2 * LSE_ATOL
