@@ -24,6 +24,11 @@ scaled by what the same counters read for a plain copy of known size); it
 is read from the committed profile summary and reported only while the
 attention sources still hash to the ones that summary was taken with.
 
+The ``overlap`` object measures the predictive draft-verify overlap on the
+same workload (rg_multibranch_attention over every request's verify rows and
+three branches, against the same rows served as separate requests, plus
+rg_plan_branches and rg_match_branches); ``--no-overlap`` skips it.
+
 ``--copy-calibration-mb N`` instead runs a plain device-to-device copy of N
 MiB a few times (for calibrating those counters) and exits.
 """
@@ -106,6 +111,124 @@ def algorithmic_work(lay):
                 draft_bytes=draft_bytes)
 
 
+
+def overlap_work(ov, branches):
+    """Bytes and flops of the overlap round's attention, counting each key of
+    a request once for all its rows (the shared-prefix access) and only the
+    allowed (query, key) pairs: verify row i sees L + i + 1 keys; a branch's
+    j-th lead row L + prefix + j + 1, its draft rows L + prefix + rows."""
+    s = ov.spec
+    D, hq, hkv = s.head_dim, s.num_q_heads, s.num_kv_heads
+    nbytes = pairs = 0
+    for r, br in enumerate(branches):
+        L, V = int(ov.ctx_len[r]), int(ov.n_verify[r])
+        n = int(ov.q_indptr[r + 1] - ov.q_indptr[r])
+        T = L + n
+        nbytes += T * hkv * D * 2 * 2 + n * hq * D * 2 * 2 + math.ceil(T / 16) * 4 + n * hq * 4
+        pairs += V * L + V * (V + 1) // 2
+        for prefix, lead, rows in br:
+            pairs += lead * (L + prefix) + lead * (lead + 1) // 2 + (rows - lead) * (L + prefix + rows)
+    return nbytes, 4 * D * hq * pairs
+
+
+def overlap_leg(lay, dev, steps, warmup, capture, timed, step_outputs):
+    """Sec. 5.1 / 5.3 measured on the step's workload: every request's rows
+    after its verify rows become overlap branches (two corrections and a
+    continuation, each with the request's draft block size), served by one
+    rg_multibranch_attention call that reads each request's keys once, and
+    -- for comparison -- the same rows and keys served as separate requests
+    (verify rows alone, each branch with its own copy of the kept prefix in
+    its page table) through rg_draft_verify_attention.  Branch planning and
+    reuse matching are timed on the step's own confidence and acceptance
+    outputs."""
+    import numpy as np
+    import torch
+
+    from paper_2609_34388_amd import binding
+    from paper_2609_34388_amd import workloads as W
+
+    branches = W.overlap_branches(lay)
+    ov = W.make_overlap_layout(lay, branches)
+    sep, origin = W.make_separate_layout(ov, branches)
+    base = W.make_attention_inputs(ov, dev)
+    kb, vb = W.make_separate_kv(ov, branches, sep, origin, base["k_cache"], base["v_cache"])
+    per_copy = sum(t.numel() * t.element_size() for t in base.values()) + \
+        kb.numel() * kb.element_size() * 2
+    copies = max(1, math.ceil(CACHE_DEFEAT_BYTES / per_copy))
+    sets = [dict(base, k_sep=kb, v_sep=vb)]
+    for _ in range(copies - 1):
+        sets.append({k: t.clone() for k, t in sets[0].items()})
+    indptr = np.concatenate([[0], np.cumsum([len(b) for b in branches])]).astype(np.int32)
+    flat = [b for br in branches for b in br]
+    col = lambda i: np.array([b[i] for b in flat], dtype=np.int32)
+    B = binding.make_branches(indptr, col(0), col(1), col(2))
+    pidx = torch.as_tensor(ov.page_indices, device=dev)
+    sidx = torch.as_tensor(sep.page_indices, device=dev)
+    lays_ov = [binding.make_layout(c["q"], c["k_cache"], ov.q_indptr, ov.n_verify, ov.ctx_len, ov.page_indptr,
+                                   pidx) for c in sets]
+    lays_sep = [binding.make_layout(c["q"], c["k_sep"], sep.q_indptr, sep.n_verify, sep.ctx_len, sep.page_indptr,
+                                    sidx) for c in sets]
+    ws_ov = torch.empty(max(16, binding.multibranch_workspace_bytes(lays_ov[0], B)), dtype=torch.uint8, device=dev)
+    ws_sep = torch.empty(max(16, binding.attention_workspace_bytes(lays_sep[0])), dtype=torch.uint8, device=dev)
+    out_ov, out_sep = torch.empty_like(base["q"]), torch.empty_like(base["q"])
+    lse_ov = torch.empty(base["q"].shape[0], ov.spec.num_q_heads, dtype=torch.float32, device=dev)
+    lse_sep = torch.empty_like(lse_ov)
+
+    def multibranch(i):
+        c = sets[i % copies]
+        binding.multibranch_attention(c["q"], c["k_cache"], c["v_cache"], lays_ov[i % copies], B, out=out_ov,
+                                      lse=lse_ov, workspace=ws_ov)
+
+    def separate(i):
+        c = sets[i % copies]
+        binding.draft_verify_attention(c["q"], c["k_sep"], c["v_sep"], None, None, None, None, sidx, out=out_sep,
+                                       lse=lse_sep, workspace=ws_sep, layout=lays_sep[i % copies])
+
+    vout, dout, draft_indptr = step_outputs
+    block_len = torch.as_tensor(np.diff(lay.draft_row_indptr).astype(np.int32), device=dev)
+    plan_out = binding.plan_branches(dout["margin"], dout["top2"], draft_indptr, 0.5)
+    cont_first = dout["top1"][:1].expand(lay.num_requests).contiguous()
+    reused = torch.empty(lay.num_requests, dtype=torch.int32, device=dev)
+
+    def plan(i):
+        binding.plan_branches(dout["margin"], dout["top2"], draft_indptr, 0.5, out=plan_out)
+
+    def match(i):
+        binding.match_branches(vout["accept_len"], vout["next_token"], block_len, plan_out, cont_first, out=reused)
+
+    for i in range(warmup):
+        multibranch(i)
+        separate(i)
+    torch.cuda.synchronize()
+    # the two paths must agree on every row (same keys, same rows)
+    multibranch(0)
+    separate(0)
+    torch.cuda.synchronize()
+    a, b = out_ov.float(), out_sep.float()
+    row_err = ((a - b).abs().amax(-1) / b.norm(dim=-1).clamp_min(1e-6)).max().item()
+    if not row_err <= 2e-2:
+        raise RuntimeError(f"multi-branch and separate-request outputs differ (max row error {row_err:.3e})")
+    mb_ms = timed(multibranch)
+    sep_ms = timed(separate)
+    plan_ms = timed(plan)
+    match_ms = timed(match)
+    ov_bytes, ov_flops = overlap_work(ov, branches)
+    sep_bytes = algorithmic_work(sep)["attn_bytes"]
+    return {
+        "branches": len(flat), "requests": lay.num_requests, "rows": ov.total_q,
+        "kv_tokens": int(ov.kv_len.sum()), "input_copies_rotated": copies,
+        "multibranch": {"us": round(mb_ms * 1e3, 3), "bytes": ov_bytes, "flops": ov_flops,
+                        "gbps": round(ov_bytes / (mb_ms * 1e-3) / 1e9, 1),
+                        "frac_hbm": round(ov_bytes / (mb_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                        "tflops": round(ov_flops / (mb_ms * 1e-3) / 1e12, 3)},
+        "separate_requests": {"us": round(sep_ms * 1e3, 3), "requests": sep.num_requests,
+                              "bytes": sep_bytes, "gbps": round(sep_bytes / (sep_ms * 1e-3) / 1e9, 1)},
+        "speedup_vs_separate": round(sep_ms / mb_ms, 3),
+        "bytes_saved": sep_bytes - ov_bytes,
+        "max_row_diff_vs_separate": float(f"{row_err:.3e}"),
+        "plan_branches_us": round(plan_ms * 1e3, 3), "match_branches_us": round(match_ms * 1e3, 3),
+    }
+
 def cpu_baseline(lay, inputs, budget_s: float):
     """The fp64 oracle as it stands, timed on this host for whole steps of
     the same workload (bounded by ``budget_s`` of CPU time)."""
@@ -145,6 +268,7 @@ def main(argv=None):
     ap.add_argument("--copies", type=int, default=0, help="input copies rotated (0 = enough for 512 MB)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-overlap", action="store_true", help="skip the overlap-round measurement")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run a plain copy of this many MiB (counter calibration) and exit")
     args = ap.parse_args(argv)
@@ -306,6 +430,9 @@ def main(argv=None):
                      "frac": round(attn_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "algorithmic_bytes": work["attn_bytes"], "us_per_call": round(attn_ms * 1e3, 3)},
     }
+    if not args.no_overlap:
+        result["overlap"] = overlap_leg(lay, dev, args.steps, args.warmup, capture, time_calls,
+                                        (vout, dout, torch.as_tensor(lay.draft_row_indptr, device=dev)))
     if not args.no_cpu_baseline:
         host = {k: base[k] for k in ("q", "k_cache", "v_cache", "verify_logits", "draft_logits", "draft_tokens")}
         sec, runs, threads, cores = cpu_baseline(lay, host, args.cpu_budget)
