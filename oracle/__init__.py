@@ -24,3 +24,10 @@ from .branches import (  # noqa: F401
     oracle_plan_branches,
     request_branches,
 )
+from .blocksize import (  # noqa: F401
+    oracle_block_state,
+    oracle_bucket,
+    oracle_plan_block_sizes,
+    oracle_route,
+    s_bin,
+)
