@@ -27,7 +27,10 @@ attention sources still hash to the ones that summary was taken with.
 The ``overlap`` object measures the predictive draft-verify overlap on the
 same workload (rg_multibranch_attention over every request's verify rows and
 three branches, against the same rows served as separate requests, plus
-rg_plan_branches and rg_match_branches); ``--no-overlap`` skips it.
+rg_plan_branches and rg_match_branches); ``--no-overlap`` skips it.  The
+``block_sizing`` object measures T_C(B) of this path at the workload's load,
+one rg_plan_block_sizes round, and the mixed-size batch it plans as one ragged
+batch, per size bucket and padded; ``--no-block-sizing`` skips it.
 
 ``--copy-calibration-mb N`` instead runs a plain device-to-device copy of N
 MiB a few times (for calibrating those counters) and exits.
@@ -229,6 +232,124 @@ def overlap_leg(lay, dev, steps, warmup, capture, timed, step_outputs):
         "plan_branches_us": round(plan_ms * 1e3, 3), "match_branches_us": round(match_ms * 1e3, 3),
     }
 
+
+def _step_calls(L, inputs, dev):
+    """A function running one step (attention + both logit passes) of batch
+    ``L`` on ``inputs``; buffers allocated once."""
+    import torch
+
+    from paper_2609_34388_amd import binding
+
+    s = L.spec
+    pidx = torch.as_tensor(L.page_indices, device=dev)
+    lt = binding.make_layout(inputs["q"], inputs["k_cache"], L.q_indptr, L.n_verify, L.ctx_len, L.page_indptr, pidx)
+    aws = torch.empty(max(16, binding.attention_workspace_bytes(lt)), dtype=torch.uint8, device=dev)
+    rws = binding.new_workspace(binding.verify_and_confidence_workspace_bytes(
+        L.num_requests, L.total_verify_rows, L.total_draft_rows, s.vocab), dev)
+    rp = torch.as_tensor(L.row_indptr, device=dev)
+    out = torch.empty_like(inputs["q"])
+    lse = torch.empty(inputs["q"].shape[0], s.num_q_heads, dtype=torch.float32, device=dev)
+    vout = dict(row_argmax=torch.empty(L.total_verify_rows, dtype=torch.int32, device=dev),
+                accept_len=torch.empty(L.num_requests, dtype=torch.int32, device=dev),
+                next_token=torch.empty(L.num_requests, dtype=torch.int32, device=dev),
+                row_entropy=torch.empty(L.total_verify_rows, dtype=torch.float32, device=dev),
+                accept_entropy=torch.empty(L.num_requests, dtype=torch.float32, device=dev))
+    dout = {k: torch.empty(L.total_draft_rows, dtype=dt, device=dev)
+            for k, dt in (("top1", torch.int32), ("top2", torch.int32), ("p1", torch.float32),
+                          ("p2", torch.float32), ("margin", torch.float32), ("entropy", torch.float32))}
+
+    def step(i):
+        binding.draft_verify_attention(inputs["q"], inputs["k_cache"], inputs["v_cache"], None, None, None, None,
+                                       pidx, out=out, lse=lse, workspace=aws, layout=lt)
+        binding.verify_and_confidence(inputs["verify_logits"], rp, inputs["draft_tokens"], inputs["draft_logits"],
+                                      workspace=rws, out_verify=vout, out_draft=dout)
+    return step
+
+
+def _gather(L, inputs, reqs):
+    """Requests ``reqs`` of batch ``L`` as a batch of their own: same K/V
+    pool, their query rows and logit rows copied out."""
+    import numpy as np
+    import torch
+
+    from paper_2609_34388_amd import workloads as W
+
+    sub = W.subset(L, reqs)
+    cat = lambda ptr: torch.as_tensor(np.concatenate([np.arange(ptr[r], ptr[r + 1]) for r in reqs]).astype(np.int64),
+                                      device=inputs["q"].device)
+    qi, vi, di = cat(L.q_indptr), cat(L.row_indptr), cat(L.draft_row_indptr)
+    return sub, dict(q=inputs["q"][qi].contiguous(), k_cache=inputs["k_cache"], v_cache=inputs["v_cache"],
+                     verify_logits=inputs["verify_logits"][vi].contiguous(),
+                     draft_tokens=inputs["draft_tokens"][vi].contiguous(),
+                     draft_logits=inputs["draft_logits"][di].contiguous())
+
+
+def block_sizing_leg(lay, dev, timed):
+    """Sec. 5.2 / 5.3 on the step's workload: T_C(B) measured for this path
+    (uniform blocks of each candidate size at this load), one planning round
+    of rg_plan_block_sizes on synthetic request states with a synthetic value
+    table, and the resulting mixed-size batch timed as one ragged batch, as
+    one batch per size bucket, and padded to the largest planned size."""
+    import numpy as np
+    import torch
+
+    from paper_2609_34388_amd import binding
+    from paper_2609_34388_amd import workloads as W
+
+    R = lay.num_requests
+    cand = list(W.BLOCK_CANDIDATES)
+
+    def batch(nv, nd):
+        L = W.with_blocks(lay, nv, nd)
+        inp = W.make_attention_inputs(L, dev)
+        inp.update(W.make_logit_inputs(L, dev))
+        return L, inp
+
+    cost_us = []
+    for B in cand:
+        L, inp = batch(np.full(R, B), np.full(R, B))
+        cost_us.append(timed(_step_calls(L, inp, dev)) * 1e3)
+        del inp
+    # rho_C: the cost of a 16-token block at this load is worth 8 tokens of progress
+    rho = 8.0 / cost_us[1]
+    d = W.make_block_policy_inputs(seed=lay.seed, num_requests=R)
+    t = lambda a, dt: torch.as_tensor(np.ascontiguousarray(a), dtype=dt, device=dev)
+    pol = binding.make_block_policy(d["candidates"], d["s_edges"], cost_us, rho, t(d["value"], torch.float32))
+    acc, ent, prev = t(d["accept_len"], torch.int32), t(d["accept_entropy"], torch.float32), t(d["prev_block"], torch.int32)
+    hist = t(d["entropy_hist"], torch.float32)
+    hist0 = hist.clone()
+    res = binding.plan_block_sizes(pol, acc, ent, prev, hist)
+    planned = res["next_block"].cpu().numpy()
+    order = res["order"].cpu().numpy()
+    offs = res["bucket_offsets"].cpu().numpy()
+
+    def plan(i):
+        hist.copy_(hist0)
+        binding.plan_block_sizes(pol, acc, ent, prev, hist, out=res)
+    plan_us = timed(plan) * 1e3
+    copy_us = timed(lambda i: hist.copy_(hist0)) * 1e3
+
+    L, inp = batch(d["prev_block"], planned)
+    ragged_us = timed(_step_calls(L, inp, dev)) * 1e3
+    parts = []
+    for b in range(len(cand)):
+        reqs = order[offs[b]:offs[b + 1]]
+        if len(reqs):
+            sub, sinp = _gather(L, inp, reqs)
+            parts.append(_step_calls(sub, sinp, dev))
+    bucketed_us = timed(lambda i: [f(i) for f in parts]) * 1e3
+    del inp, parts
+    Lp, pinp = batch(d["prev_block"], np.full(R, int(planned.max())))
+    padded_us = timed(_step_calls(Lp, pinp, dev)) * 1e3
+    del pinp
+    return {
+        "candidates": cand, "T_C_us": [round(x, 3) for x in cost_us], "rho_per_us": round(rho, 6),
+        "planned": {str(c): int((planned == c).sum()) for c in cand},
+        "plan_block_sizes_us": round(max(plan_us - copy_us, 0.0), 3),
+        "mixed_step_us": {"ragged_one_batch": round(ragged_us, 3), "bucketed": round(bucketed_us, 3),
+                          "padded_to_largest": round(padded_us, 3)},
+    }
+
 def cpu_baseline(lay, inputs, budget_s: float):
     """The fp64 oracle as it stands, timed on this host for whole steps of
     the same workload (bounded by ``budget_s`` of CPU time)."""
@@ -269,6 +390,7 @@ def main(argv=None):
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overlap", action="store_true", help="skip the overlap-round measurement")
+    ap.add_argument("--no-block-sizing", action="store_true", help="skip the block-sizing measurement")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run a plain copy of this many MiB (counter calibration) and exit")
     args = ap.parse_args(argv)
@@ -433,6 +555,8 @@ def main(argv=None):
     if not args.no_overlap:
         result["overlap"] = overlap_leg(lay, dev, args.steps, args.warmup, capture, time_calls,
                                         (vout, dout, torch.as_tensor(lay.draft_row_indptr, device=dev)))
+    if not args.no_block_sizing:
+        result["block_sizing"] = block_sizing_leg(lay, dev, time_calls)
     if not args.no_cpu_baseline:
         host = {k: base[k] for k in ("q", "k_cache", "v_cache", "verify_logits", "draft_logits", "draft_tokens")}
         sec, runs, threads, cores = cpu_baseline(lay, host, args.cpu_budget)

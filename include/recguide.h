@@ -27,6 +27,13 @@
  *   rg_plan_branches           risky positions and the branches to prepare
  *   rg_match_branches          which prepared branch a verification confirms
  *
+ * and, for verification-guided block sizing (Sec. 5.2) with block-size
+ * bucketed serving (Sec. 5.3):
+ *
+ *   rg_plan_block_sizes        each request's next draft block size from its
+ *                              verification history, and the requests grouped
+ *                              by that size
+ *
  * Conventions shared by every entry point
  * ---------------------------------------
  * - bf16 tensors are passed as their raw 16-bit patterns (uint16_t).
@@ -59,7 +66,7 @@
 extern "C" {
 #endif
 
-#define RG_ABI_VERSION 2
+#define RG_ABI_VERSION 3
 
 typedef int32_t rg_status;
 #define RG_OK 0
@@ -313,6 +320,74 @@ rg_status rg_match_branches(const int32_t* accept_len, const int32_t* next_token
                             const int32_t* n_corr, const int32_t* corr_pos, const int32_t* corr_tok,
                             const int32_t* continuation, const int32_t* cont_first, int32_t num_requests,
                             int32_t* reused, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Verification-guided block sizing and bucketing (Sec. 5.2, Sec. 5.3)
+ * ------------------------------------------------------------------------ */
+
+#define RG_BLOCK_MAX_CANDIDATES 8
+#define RG_BLOCK_MAX_S_BINS 64
+#define RG_BLOCK_MAX_REQUESTS 65536
+
+/*
+ * The block-size policy of Eq. 3 at one serving load C.
+ *
+ *   num_candidates  NB, 1 .. 8
+ *   candidates      host [NB] candidate block sizes, ascending, distinct, >= 1
+ *   num_s_bins      NS, 1 .. 64: the table's s axis is cut into NS bins
+ *   s_edges         host [NS-1] nondecreasing bin edges (NULL when NS = 1);
+ *                   bin k holds s_edges[k-1] <= s < s_edges[k]
+ *   cost            host [NB] profiled execution cost T_C(B) of each candidate
+ *   rho             the cost weight rho_C
+ *   value           DEVICE [NB][NS][NB][2] fp32 expected accepted progress
+ *                   V_B(s, z): value[b][k][j][f] for candidate b, s bin k,
+ *                   previous block size candidate j and full-acceptance flag f
+ * Unsorted or repeated candidates, or decreasing edges, give RG_ERR_SHAPE;
+ * NB or NS out of range RG_ERR_UNSUPPORTED.
+ */
+typedef struct rg_block_policy {
+  int32_t num_candidates;
+  const int32_t* candidates;
+  int32_t num_s_bins;
+  const float* s_edges;
+  const float* cost;
+  float rho;
+  const float* value;
+} rg_block_policy;
+
+/*
+ * One round of block sizing for a batch (Sec. 5.2), then the requests grouped
+ * by planned size (Sec. 5.3).  Per request r, after the verification of its
+ * block of size B_{t-1} = prev_block[r]:
+ *
+ *   s = -(accept_entropy[r] + entropy_hist[r]) / 2     (Eq. 2: e_{t-1}, e_{t-2})
+ *   j = the largest candidate index with candidates[j] <= B_{t-1} (0 if none)
+ *   f = 1 if accept_len[r] >= B_{t-1} (the block was accepted in full) else 0
+ *   next_block[r] = the candidate B maximising value[B][bin(s)][j][f] -
+ *                   rho * cost[B] (Eq. 3), the smaller candidate on ties
+ *   entropy_hist[r] = accept_entropy[r]   (the history for the next round)
+ *
+ * computed in fp32 with one rounding per operation (no fused multiply-add).
+ *
+ *   accept_len, accept_entropy  DEVICE [R] rg_verify_accept outputs of the
+ *                   round just verified (accept_entropy is its e_t)
+ *   prev_block      DEVICE [R] size of the block that round verified
+ *   entropy_hist    DEVICE [R] in: the entropy of the round before; out: the
+ *                   entropy of this round (the caller seeds new requests)
+ *   num_requests    R, 0 .. 65536
+ *   next_block      DEVICE [R] out: planned block size
+ *   order           DEVICE [R] out: request indices grouped by planned block
+ *                   size, smaller sizes first, ascending index within a size
+ *                   (a stable sort); may be NULL when R = 0
+ *   bucket_offsets  DEVICE [NB+1] out: candidate b's requests are
+ *                   order[bucket_offsets[b] .. bucket_offsets[b+1]-1];
+ *                   NULL (with order NULL) to skip the grouping
+ * One launch of one work group; no workspace.
+ */
+rg_status rg_plan_block_sizes(const rg_block_policy* policy, const int32_t* accept_len,
+                              const float* accept_entropy, const int32_t* prev_block, float* entropy_hist,
+                              int32_t num_requests, int32_t* next_block, int32_t* order,
+                              int32_t* bucket_offsets, void* stream);
 
 #ifdef __cplusplus
 }

@@ -47,6 +47,12 @@ class BranchLayout(ctypes.Structure):
                 ("lead", ctypes.c_void_p), ("rows", ctypes.c_void_p)]
 
 
+class BlockPolicy(ctypes.Structure):
+    _fields_ = [("num_candidates", ctypes.c_int32), ("candidates", ctypes.c_void_p),
+                ("num_s_bins", ctypes.c_int32), ("s_edges", ctypes.c_void_p), ("cost", ctypes.c_void_p),
+                ("rho", ctypes.c_float), ("value", ctypes.c_void_p)]
+
+
 class AttnPlanInfo(ctypes.Structure):
     _fields_ = [("num_launches", ctypes.c_int32), ("chunk_keys", ctypes.c_int32),
                 ("work_items", ctypes.c_int64), ("split_requests", ctypes.c_int64),
@@ -58,7 +64,7 @@ EXPORTS = ("rg_abi_version", "rg_status_string", "rg_draft_verify_attention_work
            "rg_verify_accept_workspace", "rg_verify_accept", "rg_draft_confidence_workspace",
            "rg_draft_confidence", "rg_verify_and_confidence_workspace", "rg_verify_and_confidence",
            "rg_multibranch_attention_workspace", "rg_multibranch_attention", "rg_plan_branches",
-           "rg_match_branches")
+           "rg_match_branches", "rg_plan_block_sizes")
 
 _LIB = None
 
@@ -90,6 +96,7 @@ def _lib():
                                            P, P, P, P, P, P, SZ, P]),
         "rg_plan_branches": (I32, [P, P, P, I32, I32, ctypes.c_float, P, P, P, P, P, P]),
         "rg_match_branches": (I32, [P, P, P, P, P, P, P, P, I32, P, P]),
+        "rg_plan_block_sizes": (I32, [ctypes.POINTER(BlockPolicy), P, P, P, P, I32, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -334,6 +341,59 @@ def match_branches(accept_len: torch.Tensor, next_token: torch.Tensor, block_len
                                   plan["corr_tok"].data_ptr(), plan["continuation"].data_ptr(),
                                   cont_first.data_ptr(), R, out.data_ptr(), _stream(stream))
     _check(st, "rg_match_branches")
+    return out
+
+
+class _BlockPolicy:
+    """An rg_block_policy with its host arrays kept alive."""
+
+    def __init__(self, candidates, s_edges, cost, rho: float, value: torch.Tensor):
+        self.candidates = np.ascontiguousarray(np.asarray(candidates), dtype=np.int32)
+        self.s_edges = np.ascontiguousarray(np.asarray(s_edges, dtype=np.float32).reshape(-1))
+        self.cost = np.ascontiguousarray(np.asarray(cost, dtype=np.float32).reshape(-1))
+        _dev(value, "value", torch.float32)
+        nb, ns = self.candidates.shape[0], self.s_edges.shape[0] + 1
+        if tuple(value.shape) != (nb, ns, nb, 2):
+            raise ValueError(f"value must be [{nb}, {ns}, {nb}, 2], got {tuple(value.shape)}")
+        if self.cost.shape[0] != nb:
+            raise ValueError("cost needs one entry per candidate")
+        self.value = value
+        self.c = BlockPolicy(nb, self.candidates.ctypes.data, ns,
+                             self.s_edges.ctypes.data if ns > 1 else None, self.cost.ctypes.data,
+                             float(rho), value.data_ptr())
+
+
+def make_block_policy(candidates, s_edges, cost, rho: float, value: torch.Tensor) -> _BlockPolicy:
+    """Policy of Eq. 3 at one load: candidate block sizes, s-bin edges, cost
+    T_C(B) per candidate (host), rho_C, and the V_B table on the device as an
+    fp32 tensor [NB, NS, NB, 2]."""
+    return _BlockPolicy(candidates, s_edges, cost, rho, value)
+
+
+def plan_block_sizes(policy: _BlockPolicy, accept_len: torch.Tensor, accept_entropy: torch.Tensor,
+                     prev_block: torch.Tensor, entropy_hist: torch.Tensor, *, bucket: bool = True,
+                     out: Optional[Dict[str, torch.Tensor]] = None, stream=None) -> Dict[str, torch.Tensor]:
+    """Next block size per request and the grouping by size
+    (rg_plan_block_sizes); entropy_hist is updated in place."""
+    _dev(accept_len, "accept_len", torch.int32)
+    _dev(accept_entropy, "accept_entropy", torch.float32)
+    _dev(prev_block, "prev_block", torch.int32)
+    _dev(entropy_hist, "entropy_hist", torch.float32)
+    R = accept_len.numel()
+    for name, t in (("accept_entropy", accept_entropy), ("prev_block", prev_block), ("entropy_hist", entropy_hist)):
+        if t.numel() != R:
+            raise ValueError(f"{name} must have {R} entries")
+    dev = accept_len.device
+    nb = policy.candidates.shape[0]
+    if out is None:
+        out = dict(next_block=torch.empty(R, dtype=torch.int32, device=dev))
+        if bucket:
+            out["order"] = torch.empty(R, dtype=torch.int32, device=dev)
+            out["bucket_offsets"] = torch.empty(nb + 1, dtype=torch.int32, device=dev)
+    st = _lib().rg_plan_block_sizes(ctypes.byref(policy.c), _ptr(accept_len), _ptr(accept_entropy),
+                                    _ptr(prev_block), _ptr(entropy_hist), R, _ptr(out["next_block"]),
+                                    _ptr(out.get("order")), _ptr(out.get("bucket_offsets")), _stream(stream))
+    _check(st, "rg_plan_block_sizes")
     return out
 
 

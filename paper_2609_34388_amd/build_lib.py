@@ -17,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(HERE, "librecguide.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ("api.cpp", "attention.hip", "logits.hip", "branches.hip")
+SOURCES = ("api.cpp", "attention.hip", "logits.hip", "branches.hip", "blocksize.hip")
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are kept out of the generated code; MFMA

@@ -15,6 +15,11 @@
 
 #include "rg_internal.h"
 
+static_assert(RG_BLOCK_MAX_CANDIDATES == rg::kMaxBlockCandidates, "header and kernel limits agree");
+static_assert(RG_BLOCK_MAX_S_BINS == rg::kMaxSBins, "header and kernel limits agree");
+static_assert(RG_BLOCK_MAX_REQUESTS == rg::kMaxBucketRequests, "header and kernel limits agree");
+static_assert(RG_BRANCH_MAX_REQS_PER_LAUNCH == rg::kMaxReqPerLaunchBr, "header and kernel limits agree");
+
 namespace {
 
 using namespace rg;
@@ -538,6 +543,50 @@ rg_status rg_match_branches(const int32_t* accept_len, const int32_t* next_token
   a.num_req = num_requests;
   a.reused = reused;
   return launch_match_branches(a, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
+
+rg_status rg_plan_block_sizes(const rg_block_policy* policy, const int32_t* accept_len,
+                              const float* accept_entropy, const int32_t* prev_block, float* entropy_hist,
+                              int32_t num_requests, int32_t* next_block, int32_t* order,
+                              int32_t* bucket_offsets, void* stream) {
+  if (!policy) return RG_ERR_NULL;
+  const int nb = policy->num_candidates, ns = policy->num_s_bins;
+  if (nb < 1 || nb > kMaxBlockCandidates || ns < 1 || ns > kMaxSBins) return RG_ERR_UNSUPPORTED;
+  if (!policy->candidates || !policy->cost || !policy->value || (ns > 1 && !policy->s_edges)) return RG_ERR_NULL;
+  for (int i = 0; i < nb; ++i) {
+    if (policy->candidates[i] < 1) return RG_ERR_SHAPE;
+    if (i > 0 && policy->candidates[i] <= policy->candidates[i - 1]) return RG_ERR_SHAPE;
+  }
+  for (int i = 1; i + 1 < ns; ++i)
+    if (!(policy->s_edges[i] >= policy->s_edges[i - 1])) return RG_ERR_SHAPE;
+  if (num_requests < 0) return RG_ERR_SHAPE;
+  if (num_requests > kMaxBucketRequests) return RG_ERR_UNSUPPORTED;
+  // grouping is asked for by bucket_offsets; order may be NULL only when there is nothing to order
+  if (order != nullptr && bucket_offsets == nullptr) return RG_ERR_NULL;
+  if (bucket_offsets != nullptr && order == nullptr && num_requests > 0) return RG_ERR_NULL;
+  if (num_requests > 0 && (!accept_len || !accept_entropy || !prev_block || !entropy_hist || !next_block))
+    return RG_ERR_NULL;
+  BlockSizeArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.nb = nb;
+  a.ns = ns;
+  for (int i = 0; i < nb; ++i) {
+    a.cand[i] = policy->candidates[i];
+    a.cost[i] = policy->cost[i];
+  }
+  for (int i = 0; i + 1 < ns; ++i) a.edges[i] = policy->s_edges[i];
+  a.rho = policy->rho;
+  a.value = policy->value;
+  a.accept_len = accept_len;
+  a.accept_entropy = accept_entropy;
+  a.prev_block = prev_block;
+  a.entropy_hist = entropy_hist;
+  a.num_req = num_requests;
+  a.next_block = next_block;
+  a.order = order;
+  a.bucket_offsets = bucket_offsets;
+  if (num_requests == 0 && bucket_offsets == nullptr) return RG_OK;
+  return launch_plan_block_sizes(a, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
 }
 
 }  // extern "C"

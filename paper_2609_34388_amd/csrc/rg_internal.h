@@ -147,4 +147,26 @@ struct MatchBranchArgs {
 hipError_t launch_plan_branches(const PlanBranchArgs& a, hipStream_t stream);
 hipError_t launch_match_branches(const MatchBranchArgs& a, hipStream_t stream);
 
+// Verification-guided block sizing and bucketing (Sec. 5.2, Sec. 5.3).
+constexpr int kMaxBlockCandidates = 8;
+constexpr int kMaxSBins = 64;
+constexpr int kMaxBucketRequests = 65536;
+struct BlockSizeArgs {
+  int32_t nb, ns;                       // candidates, s bins
+  int32_t cand[kMaxBlockCandidates];    // ascending block sizes
+  float edges[kMaxSBins - 1];           // ascending s-bin edges
+  float cost[kMaxBlockCandidates];      // T_C(B)
+  float rho;
+  const float* value;                   // [nb][ns][nb][2]
+  const int32_t* accept_len;
+  const float* accept_entropy;
+  const int32_t* prev_block;
+  float* entropy_hist;
+  int32_t num_req;
+  int32_t* next_block;
+  int32_t* order;                       // NULL when not grouping or when num_req == 0
+  int32_t* bucket_offsets;              // NULL: no grouping
+};
+hipError_t launch_plan_block_sizes(const BlockSizeArgs& a, hipStream_t stream);
+
 }  // namespace rg

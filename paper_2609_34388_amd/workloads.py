@@ -247,6 +247,30 @@ def make_overlap_layout(layout: Layout, branches, spare_pages: int = 8) -> Layou
                   used + spare_pages)
 
 
+
+def with_blocks(layout: Layout, n_verify, n_draft, spare_pages: int = 8) -> Layout:
+    """``layout``'s requests (same contexts) with new verify / draft row counts
+    and a freshly permuted page table."""
+    rng = np.random.default_rng(_seed_sequence(layout.spec, layout.seed).spawn(8)[7])
+    nv = np.asarray(n_verify, dtype=np.int32)
+    nd = np.asarray(n_draft, dtype=np.int32)
+    kv = layout.ctx_len + nv + nd
+    pages = (kv + PAGE_SIZE - 1) // PAGE_SIZE
+    used = int(pages.sum())
+    order = rng.permutation(used + spare_pages)
+    return _paged(layout, layout.ctx_len, nv, nd, _prefix(pages), order[:used], used + spare_pages)
+
+
+def subset(layout: Layout, requests) -> Layout:
+    """The listed requests of ``layout`` as a batch of their own (same
+    pages, same order of the page pool)."""
+    req = np.asarray(requests, dtype=np.int64)
+    counts = (layout.page_indptr[req + 1] - layout.page_indptr[req]).astype(np.int64)
+    idx = np.concatenate([layout.page_indices[layout.page_indptr[r]:layout.page_indptr[r + 1]] for r in req]) \
+        if len(req) else np.zeros(0, np.int32)
+    return _paged(layout, layout.ctx_len[req], layout.n_verify[req], layout.n_draft[req], _prefix(counts), idx,
+                  layout.num_pages)
+
 def make_separate_layout(overlap: Layout, branches) -> Tuple[Layout, list]:
     """The same rows served without a shared prefix: every request of
     ``overlap`` becomes one request of its verify rows plus one request per
@@ -312,6 +336,43 @@ def make_separate_kv(overlap: Layout, branches, separate: Layout, origin, k_cach
         k[dp, :, ds, :] = k_cache[sp_, :, ss, :]
         v[dp, :, :, ds] = v_cache[sp_, :, :, ss]
     return k, v
+
+
+BLOCK_CANDIDATES = (8, 16, 32)
+
+
+def make_block_policy_inputs(seed: int = 0, num_requests: int = 128, num_s_bins: int = 8,
+                             candidates=BLOCK_CANDIDATES) -> Dict[str, np.ndarray]:
+    """A synthetic block-size policy and one round of request states.
+
+    The paper calibrates its value table from model rollouts; this stand-in
+    is a smooth table of the same shape: an expected acceptance potential
+    A = 2 + 30 exp(2 s) (1.5 after a full acceptance) (B_prev / 16)^0.25 at
+    each s-bin centre, and V_B = A (1 - exp(-B / A)) -- more progress for
+    larger blocks, saturating at A -- plus N(0, 0.05) noise.  s-bin edges
+    are evenly spaced on [-4, 0].  Request states: entropies U[0, 3],
+    previous block sizes drawn from the candidates, accepted lengths
+    U{0 .. B_prev}.  Costs are left to the caller (they are measured)."""
+    rng = np.random.default_rng(np.random.SeedSequence([_SEED_TAG, 99, seed]))
+    cand = np.asarray(candidates, dtype=np.int32)
+    nb, ns = len(cand), int(num_s_bins)
+    edges = np.linspace(-4.0, 0.0, ns + 1)[1:-1].astype(np.float32) if ns > 1 else np.zeros(0, np.float32)
+    lo = np.concatenate([[-5.0], edges])
+    hi = np.concatenate([edges, [0.5]])
+    centre = 0.5 * (lo + hi)
+    value = np.zeros((nb, ns, nb, 2), dtype=np.float32)
+    for k in range(ns):
+        for j in range(nb):
+            for f in range(2):
+                A = 2.0 + 30.0 * np.exp(2.0 * centre[k]) * (1.5 if f else 1.0) * (cand[j] / 16.0) ** 0.25
+                value[:, k, j, f] = A * (1.0 - np.exp(-cand / A))
+    value += rng.normal(0.0, 0.05, size=value.shape).astype(np.float32)
+    R = int(num_requests)
+    prev = rng.choice(cand, size=R).astype(np.int32)
+    accept = np.array([rng.integers(0, p + 1) for p in prev], dtype=np.int32)
+    return dict(candidates=cand, s_edges=edges, value=value.astype(np.float32),
+                accept_len=accept, accept_entropy=rng.uniform(0, 3, R).astype(np.float32),
+                entropy_hist=rng.uniform(0, 3, R).astype(np.float32), prev_block=prev)
 
 def _gen(layout: Layout, device, stream: int) -> torch.Generator:
     ss = _seed_sequence(layout.spec, layout.seed).spawn(8)[stream]

@@ -132,6 +132,41 @@ def test_branch_plan_and_match_validation_errors():
     assert lib.rg_match_branches(d, d, d, d, d, d, d, None, 2, d, None) == 1
 
 
+def _policy(cand=(8, 16, 32), edges=(-1.0, -0.5), cost=(1.0, 2.0, 3.0), nb=None, ns=None):
+    c = np.asarray(cand, dtype=np.int32)
+    e = np.asarray(edges, dtype=np.float32)
+    k = np.asarray(cost, dtype=np.float32)
+    pol = binding.BlockPolicy(len(c) if nb is None else nb, c.ctypes.data, (len(e) + 1) if ns is None else ns,
+                              e.ctypes.data if len(e) else None, k.ctypes.data, 1.0, FAKE_DEV)
+    return pol, (c, e, k)
+
+
+def test_block_size_validation_errors():
+    lib = binding.library()
+    d = FAKE_DEV
+    args = lambda pol, R=4, order=d, offs=d: (ctypes.byref(pol), d, d, d, d, R, d, order, offs, None)
+    assert lib.rg_plan_block_sizes(None, d, d, d, d, 4, d, d, d, None) == 1
+    pol, keep = _policy(cand=(16, 8, 32))
+    assert lib.rg_plan_block_sizes(*args(pol)) == 2          # unsorted candidates
+    pol, keep = _policy(cand=(8, 8, 32))
+    assert lib.rg_plan_block_sizes(*args(pol)) == 2          # repeated candidate
+    pol, keep = _policy(cand=(0, 8, 32))
+    assert lib.rg_plan_block_sizes(*args(pol)) == 2          # block size below 1
+    pol, keep = _policy(edges=(-0.5, -1.0))
+    assert lib.rg_plan_block_sizes(*args(pol)) == 2          # decreasing edges
+    pol, keep = _policy(nb=9)
+    assert lib.rg_plan_block_sizes(*args(pol)) == 3          # too many candidates
+    pol, keep = _policy(ns=65)
+    assert lib.rg_plan_block_sizes(*args(pol)) == 3          # too many bins
+    pol, keep = _policy()
+    assert lib.rg_plan_block_sizes(*args(pol, R=-1)) == 2
+    assert lib.rg_plan_block_sizes(*args(pol, R=65537)) == 3
+    assert lib.rg_plan_block_sizes(*args(pol, order=None)) == 1   # offsets without order
+    assert lib.rg_plan_block_sizes(*args(pol, offs=None)) == 1    # order without offsets
+    assert lib.rg_plan_block_sizes(ctypes.byref(pol), d, None, d, d, 4, d, d, d, None) == 1
+    assert lib.rg_plan_block_sizes(*args(pol, R=0, order=None, offs=None)) == 0  # nothing to do
+
+
 def test_logit_validation_errors():
     lib = binding.library()
     ws = ctypes.c_void_p(0x2000)
