@@ -233,39 +233,6 @@ def overlap_leg(lay, dev, steps, warmup, capture, timed, step_outputs):
     }
 
 
-def _step_calls(L, inputs, dev):
-    """A function running one step (attention + both logit passes) of batch
-    ``L`` on ``inputs``; buffers allocated once."""
-    import torch
-
-    from paper_2609_34388_amd import binding
-
-    s = L.spec
-    pidx = torch.as_tensor(L.page_indices, device=dev)
-    lt = binding.make_layout(inputs["q"], inputs["k_cache"], L.q_indptr, L.n_verify, L.ctx_len, L.page_indptr, pidx)
-    aws = torch.empty(max(16, binding.attention_workspace_bytes(lt)), dtype=torch.uint8, device=dev)
-    rws = binding.new_workspace(binding.verify_and_confidence_workspace_bytes(
-        L.num_requests, L.total_verify_rows, L.total_draft_rows, s.vocab), dev)
-    rp = torch.as_tensor(L.row_indptr, device=dev)
-    out = torch.empty_like(inputs["q"])
-    lse = torch.empty(inputs["q"].shape[0], s.num_q_heads, dtype=torch.float32, device=dev)
-    vout = dict(row_argmax=torch.empty(L.total_verify_rows, dtype=torch.int32, device=dev),
-                accept_len=torch.empty(L.num_requests, dtype=torch.int32, device=dev),
-                next_token=torch.empty(L.num_requests, dtype=torch.int32, device=dev),
-                row_entropy=torch.empty(L.total_verify_rows, dtype=torch.float32, device=dev),
-                accept_entropy=torch.empty(L.num_requests, dtype=torch.float32, device=dev))
-    dout = {k: torch.empty(L.total_draft_rows, dtype=dt, device=dev)
-            for k, dt in (("top1", torch.int32), ("top2", torch.int32), ("p1", torch.float32),
-                          ("p2", torch.float32), ("margin", torch.float32), ("entropy", torch.float32))}
-
-    def step(i):
-        binding.draft_verify_attention(inputs["q"], inputs["k_cache"], inputs["v_cache"], None, None, None, None,
-                                       pidx, out=out, lse=lse, workspace=aws, layout=lt)
-        binding.verify_and_confidence(inputs["verify_logits"], rp, inputs["draft_tokens"], inputs["draft_logits"],
-                                      workspace=rws, out_verify=vout, out_draft=dout)
-    return step
-
-
 def _gather(L, inputs, reqs):
     """Requests ``reqs`` of batch ``L`` as a batch of their own: same K/V
     pool, their query rows and logit rows copied out."""
@@ -295,6 +262,7 @@ def block_sizing_leg(lay, dev, timed):
 
     from paper_2609_34388_amd import binding
     from paper_2609_34388_amd import workloads as W
+    from paper_2609_34388_amd.cost_profile import make_step
 
     R = lay.num_requests
     cand = list(W.BLOCK_CANDIDATES)
@@ -308,7 +276,7 @@ def block_sizing_leg(lay, dev, timed):
     cost_us = []
     for B in cand:
         L, inp = batch(np.full(R, B), np.full(R, B))
-        cost_us.append(timed(_step_calls(L, inp, dev)) * 1e3)
+        cost_us.append(timed(make_step(L, inp, dev)) * 1e3)
         del inp
     # rho_C: the cost of a 16-token block at this load is worth 8 tokens of progress
     rho = 8.0 / cost_us[1]
@@ -330,17 +298,17 @@ def block_sizing_leg(lay, dev, timed):
     copy_us = timed(lambda i: hist.copy_(hist0)) * 1e3
 
     L, inp = batch(d["prev_block"], planned)
-    ragged_us = timed(_step_calls(L, inp, dev)) * 1e3
+    ragged_us = timed(make_step(L, inp, dev)) * 1e3
     parts = []
     for b in range(len(cand)):
         reqs = order[offs[b]:offs[b + 1]]
         if len(reqs):
             sub, sinp = _gather(L, inp, reqs)
-            parts.append(_step_calls(sub, sinp, dev))
+            parts.append(make_step(sub, sinp, dev))
     bucketed_us = timed(lambda i: [f(i) for f in parts]) * 1e3
     del inp, parts
     Lp, pinp = batch(d["prev_block"], np.full(R, int(planned.max())))
-    padded_us = timed(_step_calls(Lp, pinp, dev)) * 1e3
+    padded_us = timed(make_step(Lp, pinp, dev)) * 1e3
     del pinp
     return {
         "candidates": cand, "T_C_us": [round(x, 3) for x in cost_us], "rho_per_us": round(rho, 6),
