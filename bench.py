@@ -27,7 +27,9 @@ attention sources still hash to the ones that summary was taken with.
 The ``overlap`` object measures the predictive draft-verify overlap on the
 same workload (rg_multibranch_attention over every request's verify rows and
 three branches, against the same rows served as separate requests, plus
-rg_plan_branches and rg_match_branches); ``--no-overlap`` skips it.  The
+rg_plan_branches and rg_match_branches, and the quadratic layout -- one draft
+block per hypothetical accepted length -- through the same entry point);
+``--no-overlap`` skips it.  The
 ``block_sizing`` object measures T_C(B) of this path at the workload's load,
 one rg_plan_block_sizes round, and the mixed-size batch it plans as one ragged
 batch, per size bucket and padded; ``--no-block-sizing`` skips it.
@@ -217,6 +219,32 @@ def overlap_leg(lay, dev, steps, warmup, capture, timed, step_outputs):
     match_ms = timed(match)
     ov_bytes, ov_flops = overlap_work(ov, branches)
     sep_bytes = algorithmic_work(sep)["attn_bytes"]
+    del sets, base, kb, vb
+
+    # The quadratic layout of Sec. 6.2 on the same requests: one draft block
+    # per hypothetical accepted length, through the same entry point.
+    qbr = W.quadratic_branches(lay)
+    qov = W.make_overlap_layout(lay, qbr)
+    qin = W.make_attention_inputs(qov, dev)
+    qcopies = max(1, math.ceil(CACHE_DEFEAT_BYTES / sum(t.numel() * t.element_size() for t in qin.values())))
+    qsets = [qin] + [{k: t.clone() for k, t in qin.items()} for _ in range(qcopies - 1)]
+    qflat = [b for br in qbr for b in br]
+    qptr = np.concatenate([[0], np.cumsum([len(b) for b in qbr])]).astype(np.int32)
+    qcol = lambda i: np.array([b[i] for b in qflat], dtype=np.int32)
+    QB = binding.make_branches(qptr, qcol(0), qcol(1), qcol(2))
+    qlay = binding.make_layout(qin["q"], qin["k_cache"], qov.q_indptr, qov.n_verify, qov.ctx_len, qov.page_indptr,
+                               torch.as_tensor(qov.page_indices, device=dev))
+    qws = torch.empty(max(16, binding.multibranch_workspace_bytes(qlay, QB)), dtype=torch.uint8, device=dev)
+    qout = torch.empty_like(qin["q"])
+    qlse = torch.empty(qin["q"].shape[0], qov.spec.num_q_heads, dtype=torch.float32, device=dev)
+
+    def quadratic(i):
+        c = qsets[i % qcopies]
+        binding.multibranch_attention(c["q"], c["k_cache"], c["v_cache"], qlay, QB, out=qout, lse=qlse,
+                                      workspace=qws)
+    q_ms = timed(quadratic)
+    q_bytes, q_flops = overlap_work(qov, qbr)
+    del qin, qsets
     return {
         "branches": len(flat), "requests": lay.num_requests, "rows": ov.total_q,
         "kv_tokens": int(ov.kv_len.sum()), "input_copies_rotated": copies,
@@ -230,6 +258,11 @@ def overlap_leg(lay, dev, steps, warmup, capture, timed, step_outputs):
         "bytes_saved": sep_bytes - ov_bytes,
         "max_row_diff_vs_separate": float(f"{row_err:.3e}"),
         "plan_branches_us": round(plan_ms * 1e3, 3), "match_branches_us": round(match_ms * 1e3, 3),
+        "quadratic_layout": {"branches": len(qflat), "rows": qov.total_q, "input_copies_rotated": qcopies, "us": round(q_ms * 1e3, 3),
+                             "bytes": q_bytes, "flops": q_flops,
+                             "gbps": round(q_bytes / (q_ms * 1e-3) / 1e9, 1),
+                             "tflops": round(q_flops / (q_ms * 1e-3) / 1e12, 3),
+                             "time_vs_three_branches": round(q_ms / mb_ms, 3)},
     }
 
 

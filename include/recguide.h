@@ -66,7 +66,7 @@
 extern "C" {
 #endif
 
-#define RG_ABI_VERSION 3
+#define RG_ABI_VERSION 4
 
 typedef int32_t rg_status;
 #define RG_OK 0
@@ -235,8 +235,8 @@ rg_status rg_verify_and_confidence(const uint16_t* verify_logits, int64_t verify
 /*
  * Branches of each request of a step (host arrays, read during the call).
  *
- * Request r lists branches branch_indptr[r] .. branch_indptr[r+1]-1, at most
- * three.  Its query rows (rg_attn_layout) are its n_verify[r] = V verify rows
+ * Request r lists branches branch_indptr[r] .. branch_indptr[r+1]-1.  Its
+ * query rows (rg_attn_layout) are its n_verify[r] = V verify rows
  * followed by each listed branch's rows in order, and its keys are its
  * ctx_len[r] = L cached tokens, the V verify rows, then the branch rows in
  * the same order (their K/V written to the request's pages like any token).
@@ -255,8 +255,14 @@ rg_status rg_verify_and_confidence(const uint16_t* verify_logits, int64_t verify
  *   lead           host [branch_indptr[R]], 0 .. rows (at most 15)
  *   rows           host [branch_indptr[R]], >= 1 (at most 65535); the listed
  *                  rows of a request sum to its rows after the verify rows
- * Violations give RG_ERR_SHAPE; more than three branches or a value past
- * its packing limit RG_ERR_UNSUPPORTED.
+ * A request may list any number of branches as long as all but at most two
+ * leading ones form one regular family: equal rows and lead, prefixes growing
+ * by a constant step >= 0 (up to 65535 branches, step at most 4095) -- e.g.
+ * correction and continuation branches (up to three of any shape), or one
+ * draft block per hypothetical accepted length 0 .. V (the quadratic layout
+ * of Sec. 6.2's comparison).
+ * Violations give RG_ERR_SHAPE; a list of another form or a value past its
+ * packing limit RG_ERR_UNSUPPORTED.
  */
 typedef struct rg_branch_layout {
   const int32_t* branch_indptr;

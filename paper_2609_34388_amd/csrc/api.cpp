@@ -58,6 +58,35 @@ rg_status validate_layout(const rg_attn_layout* L) {
 // Branch layout of the overlap (Sec. 5.1): at most three branches per
 // request, each within its packing limits, and a listed set of branches
 // covers exactly the request's rows after its verify rows.
+// Packs request r's branch list into at most three words plus a repeat
+// word: the longest trailing run of branches with equal rows and lead whose
+// prefixes grow by a constant step >= 0 becomes one word standing for
+// `count` branches; the branches before it keep a word each.  False when
+// more than two branches precede that run or the run exceeds the packing
+// limits.
+bool pack_branches(const rg_branch_layout* B, int r, int32_t (&w)[3], int32_t& rep) {
+  w[0] = w[1] = w[2] = 0;
+  rep = 0;
+  if (B == nullptr) return true;
+  const int k0 = B->branch_indptr[r], m = B->branch_indptr[r + 1] - k0;
+  if (m == 0) return true;
+  auto same = [&](int a, int b) { return B->rows[k0 + a] == B->rows[k0 + b] && B->lead[k0 + a] == B->lead[k0 + b]; };
+  int j = m - 1, step = 0;
+  if (m >= 2 && same(m - 1, m - 2) && B->prefix[k0 + m - 1] >= B->prefix[k0 + m - 2]) {
+    step = B->prefix[k0 + m - 1] - B->prefix[k0 + m - 2];
+    j = m - 2;
+    while (j > 0 && same(j - 1, j) && B->prefix[k0 + j] - B->prefix[k0 + j - 1] == step) --j;
+  }
+  const int count = m - j;
+  if (j > 2 || count > 0xffff || step > 0xfff) return false;
+  for (int i = 0; i <= j; ++i) {
+    const int k = k0 + i;
+    w[i] = (int32_t)((uint32_t)B->rows[k] | ((uint32_t)B->prefix[k] << 16) | ((uint32_t)B->lead[k] << 28));
+  }
+  rep = (int32_t)((uint32_t)count | ((uint32_t)step << 16) | ((uint32_t)j << 28));
+  return true;
+}
+
 rg_status validate_branches(const rg_attn_layout* L, const rg_branch_layout* B) {
   if (B == nullptr || !B->branch_indptr) return RG_ERR_NULL;
   if (B->branch_indptr[0] != 0) return RG_ERR_SHAPE;
@@ -66,7 +95,6 @@ rg_status validate_branches(const rg_attn_layout* L, const rg_branch_layout* B) 
   for (int r = 0; r < L->num_requests; ++r) {
     const int nb = B->branch_indptr[r + 1] - B->branch_indptr[r];
     if (nb < 0) return RG_ERR_SHAPE;
-    if (nb > 3) return RG_ERR_UNSUPPORTED;
     if (nb == 0) continue;
     const int64_t n = (int64_t)L->q_indptr[r + 1] - L->q_indptr[r];
     const int V = L->n_verify[r];
@@ -78,6 +106,8 @@ rg_status validate_branches(const rg_attn_layout* L, const rg_branch_layout* B) 
       sum += B->rows[k];
     }
     if (sum != n - V) return RG_ERR_SHAPE;
+    int32_t w[3], rep;
+    if (!pack_branches(B, r, w, rep)) return RG_ERR_UNSUPPORTED;
   }
   return RG_OK;
 }
@@ -136,12 +166,6 @@ int choose_chunk(const std::vector<int64_t>& pair_keys) {
 
 // Branch words of request r (see AttnReqBr); all zero when B is NULL or
 // the request lists no branch.
-void branch_words(const rg_branch_layout* B, int r, int32_t (&w)[3]) {
-  w[0] = w[1] = w[2] = 0;
-  if (B == nullptr) return;
-  for (int k = B->branch_indptr[r], j = 0; k < B->branch_indptr[r + 1]; ++k, ++j)
-    w[j] = (int32_t)((uint32_t)B->rows[k] | ((uint32_t)B->prefix[k] << 16) | ((uint32_t)B->lead[k] << 28));
-}
 
 template <typename Plan, int MaxReq>
 rg_status plan_attention(const rg_attn_layout* L, const rg_branch_layout* B, FullPlanT<Plan>& fp) {
@@ -177,7 +201,7 @@ rg_status plan_attention(const rg_attn_layout* L, const rg_branch_layout* B, Ful
       const int r = order[r0 + k];
       const int64_t n = L->q_indptr[r + 1] - L->q_indptr[r];
       auto& q = p.req[k];
-      if constexpr (__is_same(Plan, AttnPlanBr)) branch_words(B, r, q.br);
+      if constexpr (__is_same(Plan, AttnPlanBr)) pack_branches(B, r, q.br, q.rep);
       q.q_start = L->q_indptr[r];
       q.ctx = L->ctx_len[r];
       q.nv = (int32_t)(n | ((int64_t)L->n_verify[r] << 16));

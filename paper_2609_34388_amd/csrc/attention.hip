@@ -233,20 +233,27 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, Plan p) 
   } else {
     int t = tok - nver, start = L + nver, prefix = nver, lead = 0, rows = n - nver;
     if constexpr (BR) {
+      // Word `last` stands for `cnt` branches of its shape whose prefixes
+      // grow by `stp`; the words before it for one branch each.
+      const int cnt = rq.rep & 0xffff, stp = (rq.rep >> 16) & 0xfff, last = (int)((uint32_t)rq.rep >> 28);
       bool found = false;
 #pragma unroll
       for (int bb = 0; bb < 3; ++bb) {
         const int w = rq.br[bb];
         const int rb = w & 0xffff;
         if (w != 0 && !found) {
-          if (t < rb) {
-            prefix = (w >> 16) & 0xfff;
+          const int span = bb == last ? rb * cnt : rb;
+          if (t < span) {
+            const int k = bb == last ? t / rb : 0;
+            t -= k * rb;
+            start += k * rb;
+            prefix = ((w >> 16) & 0xfff) + k * stp;
             lead = (int)((uint32_t)w >> 28);
             rows = rb;
             found = true;
           } else {
-            t -= rb;
-            start += rb;
+            t -= span;
+            start += span;
           }
         }
       }

@@ -28,12 +28,17 @@ struct AttnReq {
 };
 
 // A request of a launch with overlap branches: its rows after the verify
-// rows are up to three branches, each packed as rows (bits 0-15) | prefix
-// verify rows kept (bits 16-27) | committed lead rows (bits 28-31); br[0] = 0
-// means no branch list (the rows after the verify rows are one
+// rows are branches, described by up to three words, each packed as rows
+// (bits 0-15) | prefix verify rows kept (bits 16-27) | committed lead rows
+// (bits 28-31), and `rep`: the word at index rep >> 28 stands for
+// rep & 0xffff branches of its shape whose prefixes grow by
+// (rep >> 16) & 0xfff each (a regular family, e.g. one draft block per
+// hypothetical accepted length); the other words for one branch each.
+// br[0] = 0 means no branch list (the rows after the verify rows are one
 // continuation block that keeps every verify row).
 struct AttnReqBr : AttnReq {
   int32_t br[3];
+  int32_t rep;
 };
 constexpr int kMaxReqPerLaunchBr = 64;  // equals RG_BRANCH_MAX_REQS_PER_LAUNCH
 

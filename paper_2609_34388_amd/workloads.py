@@ -223,6 +223,19 @@ def overlap_branches(layout: Layout):
     return out
 
 
+
+def quadratic_branches(layout: Layout):
+    """The quadratic speculative layout the paper contrasts RecGuide with
+    (Sec. 6.2): for each request, one B-row draft block per hypothetical
+    accepted length a = 0 .. V of the block under verification, each keeping
+    the first a verify rows and supplying no correction token --
+    (prefix = a, lead = 0, rows = B) for every a; (V + 1) B rows in all."""
+    out = []
+    for r in range(layout.num_requests):
+        V, B = int(layout.n_verify[r]), int(layout.n_draft[r])
+        out.append([(a, 0, B) for a in range(V + 1)] if B else [])
+    return out
+
 def _paged(layout: Layout, ctx_len, n_verify, n_draft, page_indptr, page_indices, num_pages) -> Layout:
     z = np.zeros(len(ctx_len), dtype=np.int32)
     ctx_len, n_verify, n_draft = (np.asarray(a, dtype=np.int32) for a in (ctx_len, n_verify, n_draft))

@@ -110,8 +110,12 @@ def test_multibranch_validation_errors():
     assert _mb_ws(l, _br([0, 2, 3], [1, 3, 0], [3, 0, 0], [2, 2, 5]))[0] == 2   # lead past rows
     assert _mb_ws(l, _br([0, 2, 3], [1, 3, 0], [1, 0, 0], [0, 4, 5]))[0] == 2   # empty branch
     assert _mb_ws(l, _br([1, 2, 3], [1, 3, 0], [1, 0, 0], [2, 2, 5]))[0] == 2   # branch_indptr[0] != 0
-    four = _br([0, 4, 5], [0, 1, 2, 3, 0], [0, 0, 0, 0, 0], [1, 1, 1, 1, 5])
-    assert _mb_ws(l, four)[0] == 3                               # at most three branches
+    family = _br([0, 4, 5], [0, 1, 2, 3, 0], [0, 0, 0, 0, 0], [1, 1, 1, 1, 5])
+    assert _mb_ws(l, family)[0] == 0                             # a regular family packs into one word
+    mixed = _br([0, 4, 5], [3, 0, 1, 3, 0], [0, 0, 0, 0, 0], [1, 1, 1, 1, 5])
+    assert _mb_ws(l, mixed)[0] == 0                              # two single words, then a family of two
+    four = _br([0, 4, 5], [3, 0, 2, 1, 0], [0, 0, 0, 0, 0], [1, 1, 1, 1, 5])
+    assert _mb_ws(l, four)[0] == 3                               # three single branches before the last
     big = _L(R=1, nv=(4100,), n=(4101,), ctx=(0,))
     assert _mb_ws(big, _br([0, 1], [4100], [0], [1]))[0] == 3    # prefix past its 12-bit field
     assert lib.rg_multibranch_attention_workspace(ctypes.byref(l.c), None, ctypes.byref(ctypes.c_size_t())) == 1

@@ -91,6 +91,10 @@ CASES = {
     # chunk boundaries between a branch's kept prefix and its own rows (the
     # first branch spans more keys than any chunk)
     "gap": ([3000, 700], [4, 2], [[(0, 0, 600), (1, 1, 5), (4, 0, 7)], [(0, 1, 300), (2, 0, 3)]]),
+    # one draft block per hypothetical accepted length (a regular family of V + 1 branches)
+    "quadratic": ([260, 31], [8, 3], [[(a, 0, 4) for a in range(9)], [(a, 0, 5) for a in range(4)]]),
+    # two single branches, then a family with prefix step 2 and lead rows
+    "family": ([500], [9], [[(4, 1, 3), (0, 0, 2)] + [(a, 1, 3) for a in range(1, 10, 2)]]),
 }
 
 
@@ -228,3 +232,21 @@ def test_overlap_round_full_size(workload):
     err = ((a - b).abs().amax(-1) / b.norm(dim=-1).clamp_min(1e-6)).max().item()
     assert err <= 2 * ATOL_ROW
     assert (lse.double() - lse_s.double()).abs().max().item() <= 2 * LSE_ATOL
+
+
+def test_quadratic_layout_full_size_low_shape():
+    """The batch-1 shape (4096 context tokens, V = B = 16, 32 / 8 heads) in the
+    quadratic layout: 17 draft blocks of 16 rows, 288 rows in all, so five
+    256-column groups; sampled heads against the oracle."""
+    lay = W.make_layout("low", seed=6)
+    branches = W.quadratic_branches(lay)
+    ov = W.make_overlap_layout(lay, branches)
+    assert ov.total_q == 16 + 17 * 16
+    inp = W.make_attention_inputs(ov, DEV, poison=float("nan"))
+    out, lse = _run(ov, inp, branches)
+    heads = [0, 17, 31]
+    ref = oracle.oracle_branch_attention(W.bf16_bits(inp["q"]), W.bf16_bits(inp["k_cache"]),
+                                         W.bf16_bits(inp["v_cache"]), ov.q_indptr, ov.n_verify, ov.ctx_len,
+                                         ov.page_indptr, ov.page_indices, branches, heads=heads)
+    for h in heads:
+        _check(out[:, h:h + 1], lse[:, h:h + 1], dict(out=ref["out"][:, h:h + 1], lse=ref["lse"][:, h:h + 1]))
