@@ -173,8 +173,8 @@ def overlap_leg(lay, dev, steps, warmup, capture, timed, step_outputs):
                                    pidx) for c in sets]
     lays_sep = [binding.make_layout(c["q"], c["k_sep"], sep.q_indptr, sep.n_verify, sep.ctx_len, sep.page_indptr,
                                     sidx) for c in sets]
-    ws_ov = torch.empty(max(16, binding.multibranch_workspace_bytes(lays_ov[0], B)), dtype=torch.uint8, device=dev)
-    ws_sep = torch.empty(max(16, binding.attention_workspace_bytes(lays_sep[0])), dtype=torch.uint8, device=dev)
+    ws_ov = binding.new_workspace(binding.multibranch_workspace_bytes(lays_ov[0], B), dev)
+    ws_sep = binding.new_workspace(binding.attention_workspace_bytes(lays_sep[0]), dev)
     out_ov, out_sep = torch.empty_like(base["q"]), torch.empty_like(base["q"])
     lse_ov = torch.empty(base["q"].shape[0], ov.spec.num_q_heads, dtype=torch.float32, device=dev)
     lse_sep = torch.empty_like(lse_ov)
@@ -234,7 +234,7 @@ def overlap_leg(lay, dev, steps, warmup, capture, timed, step_outputs):
     QB = binding.make_branches(qptr, qcol(0), qcol(1), qcol(2))
     qlay = binding.make_layout(qin["q"], qin["k_cache"], qov.q_indptr, qov.n_verify, qov.ctx_len, qov.page_indptr,
                                torch.as_tensor(qov.page_indices, device=dev))
-    qws = torch.empty(max(16, binding.multibranch_workspace_bytes(qlay, QB)), dtype=torch.uint8, device=dev)
+    qws = binding.new_workspace(binding.multibranch_workspace_bytes(qlay, QB), dev)
     qout = torch.empty_like(qin["q"])
     qlse = torch.empty(qin["q"].shape[0], qov.spec.num_q_heads, dtype=torch.float32, device=dev)
 
@@ -427,7 +427,7 @@ def main(argv=None):
 
     layouts = [binding.make_layout(c["q"], c["k_cache"], lay.q_indptr, lay.n_verify, lay.ctx_len,
                                    lay.page_indptr, page_idx) for c in sets]
-    attn_ws = torch.empty(max(16, binding.attention_workspace_bytes(layouts[0])), dtype=torch.uint8, device=dev)
+    attn_ws = binding.new_workspace(binding.attention_workspace_bytes(layouts[0]), dev)
     ver_ws = binding.new_workspace(binding.verify_accept_workspace_bytes(
         lay.num_requests, lay.total_verify_rows, s.vocab), dev)
     dr_ws = binding.new_workspace(binding.draft_confidence_workspace_bytes(lay.total_draft_rows, s.vocab), dev)
@@ -553,6 +553,22 @@ def main(argv=None):
                      "frac": round(attn_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "algorithmic_bytes": work["attn_bytes"], "us_per_call": round(attn_ms * 1e3, 3)},
     }
+    if plan["split_requests"] > 0:
+        # The one-launch work-queue mode (split chunks merged in the same
+        # launch), opt-in through RG_ATTN_PERSIST=1, timed the same way.
+        prev = os.environ.get("RG_ATTN_PERSIST")
+        os.environ["RG_ATTN_PERSIST"] = "1"
+        try:
+            one_ms = time_calls(attention)
+            one_plan = binding.attention_plan(layouts[0])
+        finally:
+            if prev is None:
+                del os.environ["RG_ATTN_PERSIST"]
+            else:
+                os.environ["RG_ATTN_PERSIST"] = prev
+        result["attention_one_launch"] = {"us": round(one_ms * 1e3, 3),
+                                          "persistent_launches": one_plan["persistent_launches"],
+                                          "time_vs_two_launches": round(one_ms / attn_ms, 3)}
     if not args.no_overlap:
         result["overlap"] = overlap_leg(lay, dev, args.steps, args.warmup, capture, time_calls,
                                         (vout, dout, torch.as_tensor(lay.draft_row_indptr, device=dev)))

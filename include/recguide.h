@@ -51,9 +51,12 @@
  *   valid once the stream reaches that point.  A failed launch returns
  *   RG_ERR_HIP.
  * - Workspaces: size them with the matching *_workspace query (same
- *   arguments).  Their contents need no initialisation and are meaningless
- *   after the call.  Two calls in flight at once must not share a
- *   workspace.
+ *   arguments).  An attention workspace (rg_draft_verify_attention,
+ *   rg_multibranch_attention) must be all zero before its first use; each
+ *   call leaves it ready for the next one (its synchronisation words return
+ *   to zero), so zeroing it once when it is allocated is enough.  The other
+ *   workspaces need no initialisation.  Contents are otherwise meaningless
+ *   after a call.  Two calls in flight at once must not share a workspace.
  * - Inputs must be finite.
  */
 #ifndef RECGUIDE_H
@@ -66,7 +69,7 @@
 extern "C" {
 #endif
 
-#define RG_ABI_VERSION 4
+#define RG_ABI_VERSION 5
 
 typedef int32_t rg_status;
 #define RG_OK 0
@@ -123,7 +126,8 @@ typedef struct rg_attn_layout {
 } rg_attn_layout;
 
 /* Workspace bytes rg_draft_verify_attention needs for this layout (0 if no
- * request is split across several KV chunks). */
+ * request is split across several KV chunks).  Zero it before its first use
+ * (see the conventions above). */
 rg_status rg_draft_verify_attention_workspace(const rg_attn_layout* layout, size_t* bytes);
 
 /*
@@ -135,7 +139,21 @@ rg_status rg_draft_verify_attention_workspace(const rg_attn_layout* layout, size
  *   lse   DEVICE [q_indptr[R]][Hq] fp32 natural-log log-sum-exp of the
  *         scaled, masked scores, or NULL
  *   ws    DEVICE workspace of at least the queried size (may be NULL when
- *         that size is 0).
+ *         that size is 0), zero before its first use.
+ *
+ * Requests whose keys are split over several KV chunks need their chunks'
+ * partial results merged: by default a second kernel does it after the main
+ * one.  With the environment variable RG_ATTN_PERSIST=1 such a launch runs
+ * instead as one work-queue launch (the library's variant of mapping mixed
+ * ragged attention work onto the compute units, Sec. 5.3): at most one work
+ * group per compute unit takes the work items (request, KV head, column
+ * group, chunk; longest request first) and then the merge items from an
+ * atomic queue, and a merge item starts as soon as the chunks it merges are
+ * done.  It gives the same results within rounding and measured slower on
+ * MI355X.  The workspace opens with the queue and per-merge counters, at the
+ * same place and size for every layout, so one workspace (zeroed once) may
+ * serve calls with different layouts one after another.  A launch with more
+ * than 16384 merge items always uses the two kernels.
  */
 rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t* q,
                                     const uint16_t* k_cache, const uint16_t* v_cache,
@@ -151,6 +169,11 @@ typedef struct rg_attn_plan_info {
   int64_t split_requests;   /* requests whose keys span more than one chunk  */
   int64_t partial_columns;  /* partial rows written to the workspace         */
   int64_t workspace_bytes;
+  int32_t persistent_launches; /* launches run as one work-queue launch      */
+  int32_t sync_words;       /* int32 synchronisation words at sync_offset    */
+  int64_t sync_offset;      /* their byte offset in the workspace (-1 without
+                               a workspace); word 2 is nonzero if a merge
+                               item ever gave up waiting (never expected)   */
 } rg_attn_plan_info;
 rg_status rg_draft_verify_attention_plan(const rg_attn_layout* layout, rg_attn_plan_info* info);
 

@@ -56,7 +56,9 @@ class BlockPolicy(ctypes.Structure):
 class AttnPlanInfo(ctypes.Structure):
     _fields_ = [("num_launches", ctypes.c_int32), ("chunk_keys", ctypes.c_int32),
                 ("work_items", ctypes.c_int64), ("split_requests", ctypes.c_int64),
-                ("partial_columns", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64)]
+                ("partial_columns", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
+                ("persistent_launches", ctypes.c_int32), ("sync_words", ctypes.c_int32),
+                ("sync_offset", ctypes.c_int64)]
 
 
 EXPORTS = ("rg_abi_version", "rg_status_string", "rg_draft_verify_attention_workspace",
@@ -228,7 +230,7 @@ def draft_verify_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torc
         _dev(lse, "lse", torch.float32)
     need = attention_workspace_bytes(lay)
     if workspace is None and need:
-        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        workspace = new_workspace(need, q.device)
     ws_ptr = _ptr(workspace) if workspace is not None else None
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     st = _lib().rg_draft_verify_attention(ctypes.byref(lay.c), q.data_ptr(), k_cache.data_ptr(),
@@ -291,7 +293,7 @@ def multibranch_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch
         _dev(lse, "lse", torch.float32)
     need = multibranch_workspace_bytes(layout, branches)
     if workspace is None and need:
-        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        workspace = new_workspace(need, q.device)
     ws_ptr = _ptr(workspace) if workspace is not None else None
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     st = _lib().rg_multibranch_attention(ctypes.byref(layout.c), ctypes.byref(branches.c), q.data_ptr(),
@@ -412,8 +414,10 @@ def draft_confidence_workspace_bytes(total_rows: int, vocab: int) -> int:
 
 
 def new_workspace(nbytes: int, device) -> torch.Tensor:
-    """A workspace of at least `nbytes` bytes (contents need no initialisation)."""
-    return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)
+    """A zeroed workspace of at least `nbytes` bytes.  Attention workspaces must be
+    zero before their first use (each call leaves them ready for the next); the
+    others need no initialisation."""
+    return torch.zeros(max(int(nbytes), 16), dtype=torch.uint8, device=device)
 
 
 def verify_accept(logits: torch.Tensor, row_indptr: torch.Tensor, draft_tokens: torch.Tensor, *,

@@ -33,7 +33,7 @@ def make_step(L, inputs, dev):
     s = L.spec
     pidx = torch.as_tensor(L.page_indices, device=dev)
     lt = binding.make_layout(inputs["q"], inputs["k_cache"], L.q_indptr, L.n_verify, L.ctx_len, L.page_indptr, pidx)
-    aws = torch.empty(max(16, binding.attention_workspace_bytes(lt)), dtype=torch.uint8, device=dev)
+    aws = binding.new_workspace(binding.attention_workspace_bytes(lt), dev)
     rws = binding.new_workspace(binding.verify_and_confidence_workspace_bytes(
         L.num_requests, L.total_verify_rows, L.total_draft_rows, s.vocab), dev)
     rp = torch.as_tensor(L.row_indptr, device=dev)

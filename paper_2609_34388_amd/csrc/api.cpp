@@ -118,9 +118,25 @@ struct FullPlanT {
   int chunk = 0;
   int cols_per_group = 256;
   int64_t items = 0, split_requests = 0, max_partial_cols = 0, total_partial_cols = 0;
+  int64_t max_comb = 0;
+  int persistent_launches = 0;
   size_t ws_bytes = 0;
+  size_t o_offset = 0;
   size_t ml_offset = 0;
+  size_t sync_offset = 0;
 };
+
+// Compute units of the current device (the one-launch kernel's work groups,
+// one per CU); 256 (MI355X) when the runtime cannot say.
+int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n <= 0) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  return n;
+}
 
 // Keys per work item.  An item costs a fixed start-up and wind-down (request
 // lookup, page numbers, first copies, epilogue: several microseconds) besides
@@ -167,9 +183,19 @@ int choose_chunk(const std::vector<int64_t>& pair_keys) {
 // Branch words of request r (see AttnReqBr); all zero when B is NULL or
 // the request lists no branch.
 
+// Launches with a split request run as the main kernel plus the combine
+// kernel, or, with RG_ATTN_PERSIST=1, as one work-queue launch (main items,
+// then the combine items; `num_cus` work groups at most).  The two launches
+// are the default because they measured faster on MI355X at every workload:
+// the device-scope counting and waiting that replaces the kernel boundary
+// costs about as much as the boundary itself.
 template <typename Plan, int MaxReq>
-rg_status plan_attention(const rg_attn_layout* L, const rg_branch_layout* B, FullPlanT<Plan>& fp) {
+rg_status plan_attention(const rg_attn_layout* L, const rg_branch_layout* B, FullPlanT<Plan>& fp,
+                         int num_cus) {
   const int R = L->num_requests;
+  const bool persist = env_int("RG_ATTN_PERSIST", 0) != 0;
+  // 16-byte rows per combine item: 128 (combine kernel), 256 (one-launch kernel)
+  const int comb_rows = persist ? 256 : 128;
   const int g = L->num_q_heads / L->num_kv_heads;
   const int hkv = L->num_kv_heads;
   fp.cols_per_group = 256;  // 8 waves x 32 columns per work group
@@ -219,7 +245,7 @@ rg_status plan_attention(const rg_attn_layout* L, const rg_branch_layout* B, Ful
         p.max_chunks = std::max<int32_t>(p.max_chunks, (int32_t)nch);
         // partials are stored per 32-column tile, so columns round up to 32
         part += hkv * nch * round_up(M, 32);
-        comb += hkv * ((M + 31) / 32) * (L->head_dim / 32);  // 128-thread slices of a tile
+        comb += hkv * ((M + 31) / 32) * (L->head_dim * 4 / comb_rows);  // slices of a tile's 4 D rows
         fp.split_requests += 1;
       }
       if (items > INT32_MAX / 2 || part > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
@@ -231,14 +257,26 @@ rg_status plan_attention(const rg_attn_layout* L, const rg_branch_layout* B, Ful
     p.total_comb = (int32_t)comb;
     p.grid_items = (int32_t)round_up(items, 8);
     p.grid_comb = (int32_t)round_up(comb, 8);
+    if (persist && comb > 0 && comb <= kMaxSyncComb) {
+      p.persist_grid = (int32_t)round_up(std::min<int64_t>(items + comb, std::max(8, num_cus)), 8);
+      fp.persistent_launches += 1;
+    }
     fp.items += items;
     fp.max_partial_cols = std::max(fp.max_partial_cols, part);
     fp.total_partial_cols += part;
+    fp.max_comb = std::max(fp.max_comb, comb);
     fp.launches.push_back(p);
   }
+  // Workspace: the one-launch kernel's synchronisation words first, at a
+  // fixed place and size (zero before the first call; every call leaves them
+  // zero, whatever its layout), then the partial outputs and their (max, sum).
+  const size_t sync_bytes = align256((size_t)kSyncWords * sizeof(int32_t));
   const size_t o_bytes = align256((size_t)fp.max_partial_cols * L->head_dim * sizeof(uint16_t));
-  fp.ml_offset = o_bytes;
-  fp.ws_bytes = fp.max_partial_cols ? o_bytes + align256((size_t)fp.max_partial_cols * 2 * sizeof(float)) : 0;
+  const size_t ml_bytes = align256((size_t)fp.max_partial_cols * 2 * sizeof(float));
+  fp.sync_offset = 0;
+  fp.o_offset = sync_bytes;
+  fp.ml_offset = sync_bytes + o_bytes;
+  fp.ws_bytes = fp.max_partial_cols ? sync_bytes + o_bytes + ml_bytes : 0;
   return RG_OK;
 }
 
@@ -276,13 +314,14 @@ namespace {
 using FullPlan = FullPlanT<AttnPlan>;
 using FullPlanBr = FullPlanT<AttnPlanBr>;
 
-rg_status plan_plain(const rg_attn_layout* layout, FullPlan& fp) {
-  return plan_attention<AttnPlan, kMaxReqPerLaunch>(layout, nullptr, fp);
+rg_status plan_plain(const rg_attn_layout* layout, FullPlan& fp, int num_cus = 256) {
+  return plan_attention<AttnPlan, kMaxReqPerLaunch>(layout, nullptr, fp, num_cus);
 }
-rg_status plan_branched(const rg_attn_layout* layout, const rg_branch_layout* branches, FullPlanBr& fp) {
+rg_status plan_branched(const rg_attn_layout* layout, const rg_branch_layout* branches, FullPlanBr& fp,
+                        int num_cus = 256) {
   rg_status st = validate_branches(layout, branches);
   if (st != RG_OK) return st;
-  return plan_attention<AttnPlanBr, kMaxReqPerLaunchBr>(layout, branches, fp);
+  return plan_attention<AttnPlanBr, kMaxReqPerLaunchBr>(layout, branches, fp, num_cus);
 }
 
 template <typename Plan>
@@ -302,8 +341,9 @@ rg_status run_attention(const rg_attn_layout* layout, const FullPlanT<Plan>& fp,
   a.out = out;
   a.lse = lse;
   a.page_indices = layout->page_indices;
-  a.part_o = fp.ws_bytes ? static_cast<uint16_t*>(ws) : nullptr;
+  a.part_o = fp.ws_bytes ? reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + fp.o_offset) : nullptr;
   a.part_ml = fp.ws_bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + fp.ml_offset) : nullptr;
+  a.sync = fp.ws_bytes ? reinterpret_cast<int32_t*>(static_cast<char*>(ws) + fp.sync_offset) : nullptr;
   a.hq = layout->num_q_heads;
   a.hkv = layout->num_kv_heads;
   a.g = layout->num_q_heads / layout->num_kv_heads;
@@ -346,6 +386,9 @@ rg_status rg_draft_verify_attention_plan(const rg_attn_layout* layout, rg_attn_p
   info->split_requests = fp.split_requests;
   info->partial_columns = fp.total_partial_cols;
   info->workspace_bytes = (int64_t)fp.ws_bytes;
+  info->persistent_launches = fp.persistent_launches;
+  info->sync_words = fp.ws_bytes ? kSyncWords : 0;
+  info->sync_offset = fp.ws_bytes ? (int64_t)fp.sync_offset : -1;
   return RG_OK;
 }
 
@@ -356,7 +399,7 @@ rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t
   rg_status st = validate_layout(layout);
   if (st != RG_OK) return st;
   FullPlan fp;
-  st = plan_plain(layout, fp);
+  st = plan_plain(layout, fp, device_cus());
   if (st != RG_OK) return st;
   return run_attention(layout, fp, q, k_cache, v_cache, out, lse, ws, ws_bytes, stream);
 }
@@ -379,7 +422,7 @@ rg_status rg_multibranch_attention(const rg_attn_layout* layout, const rg_branch
   rg_status st = validate_layout(layout);
   if (st != RG_OK) return st;
   FullPlanBr fp;
-  st = plan_branched(layout, branches, fp);
+  st = plan_branched(layout, branches, fp, device_cus());
   if (st != RG_OK) return st;
   return run_attention(layout, fp, q, k_cache, v_cache, out, lse, ws, ws_bytes, stream);
 }

@@ -118,6 +118,35 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// Device-coherent stores and loads (agent-scope relaxed atomics: the stores
+// write through to the level all XCDs share, the loads read from it), used
+// for the split-KV partials that a combine item of the same launch reads,
+// possibly on another XCD.  Ordering between a wave's stores and the count it
+// publishes afterwards comes from waiting for the stores to complete
+// (vmcnt 0) before the counting atomic; the reader's loads are issued only
+// after it has seen the full count.  No cache-wide write-back or invalidate
+// is needed, because only these locations are shared.
+__device__ __forceinline__ void store16_coherent(uint16_t* p, u32x4 w) {
+  uint64_t* q = reinterpret_cast<uint64_t*>(p);
+  __hip_atomic_store(q, (uint64_t)w[0] | ((uint64_t)w[1] << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(q + 1, (uint64_t)w[2] | ((uint64_t)w[3] << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store8_coherent(float* p, float x, float y) {
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p),
+                     (uint64_t)__float_as_uint(x) | ((uint64_t)__float_as_uint(y) << 32), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ u32x4 load16_coherent(const uint16_t* p) {
+  const uint64_t* q = reinterpret_cast<const uint64_t*>(p);
+  const uint64_t lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t hi = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return u32x4{(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)};
+}
+__device__ __forceinline__ float2 load8_coherent(const float* p) {
+  const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+}
+
 constexpr int kWaves = 8;      // compute waves per work group (two per SIMD)
 constexpr int kProducers = 4;  // copy waves per work group (one per SIMD)
 constexpr int kThreads = 64 * (kWaves + kProducers);
@@ -138,8 +167,13 @@ static_assert(kSuper % kKeyTile == 0, "a super-tile is a whole number of key til
 // accepts a 1 KiB LDS-DMA instruction only every few dozen cycles, and a
 // compute wave issuing its share would stall for most of a buffer's worth of
 // them instead of computing.
-template <int D, typename Plan>
-__global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, Plan p) {
+//
+// PERSIST: the item runs inside the one-launch work-queue kernel.  Every wave
+// then passes the same barriers (the copy waves join the key-group merge),
+// and a split item's partials are stored device-coherently and counted so
+// that the combine items of the same launch can merge them.
+template <int D, typename Plan, bool PERSIST>
+__device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, const int item, uint16_t* lds) {
   constexpr bool BR = __is_same(Plan, AttnPlanBr);  // rows after the verify rows form branches
   constexpr int NCH = D / 8;                   // 16-byte chunks per K row
   constexpr int KSTEPS = D / 16;               // MFMA k-steps of q.k
@@ -157,15 +191,9 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, Plan p) 
   // vbuf[b] = V of 8 pages ([page][D][16 keys], halves swizzled per row).
   // K runs two buffers ahead and V one: a buffer's K is issued a whole
   // buffer period before it is needed, with 160 KiB of LDS in all.
-  __shared__ __attribute__((aligned(16))) uint16_t lds[(kKBufs + kVBufs) * SUPER];
   auto kbuf = [&](int s) { return lds + (s % kKBufs) * SUPER; };
   auto vbuf = [&](int s) { return lds + (kKBufs + s % kVBufs) * SUPER; };
 
-  // One request: its heads' chunk ranges go to one XCD each (shared q and
-  // page list in that XCD's L2).  Several: dispatch order, so the longest
-  // requests, which come first, spread over all XCDs.
-  const int item = p.num_req == 1 ? xcd_item(p.grid_items) : (int)blockIdx.x;
-  if (item >= p.total_items) return;
   const int r = find_request(p, item, false);
   const auto rq = p.req[r];
   const int n = rq.nv & 0xffff, nver = rq.nv >> 16, L = rq.ctx, T = L + n;
@@ -450,6 +478,12 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, Plan p) 
         issue_v(s + 1);  // into the V buffer of s - 1
       }
     }
+    if constexpr (PERSIST) {
+      if (nct < 8) {  // the key-group merge's two barriers
+        lds_barrier();
+        lds_barrier();
+      }
+    }
     return;
   }
   for (int s = 0; s < nsup; ++s) {
@@ -507,9 +541,9 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, Plan p) 
   }
 
   // Epilogue.
-  if (!valid) return;
-  const size_t orow = (size_t)(rq.q_start + tok) * a.hq + hk * g + hh;
   if (nch == 1) {
+    if (!valid) return;
+    const size_t orow = (size_t)(rq.q_start + tok) * a.hq + hk * g + hh;
     const float inv = 1.f / l_tot;
     uint16_t* dst = a.out + orow * D;
     for (int dt = 0; dt < DT; ++dt)
@@ -528,38 +562,62 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, Plan p) 
     // own order: 16-byte row (dt, j) of lane l (its registers 8 j .. 8 j + 7)
     // at ((dt * 2 + j) * 64 + l) * 16 bytes, so every store instruction writes
     // 1 KiB contiguously.
+    // In the one-launch kernel the stores are device-coherent (they reach
+    // the point every XCD reads from before the wave's wait below ends), and
+    // then the wave adds its tile to the column group's finished count.
     const int M32 = (M + 31) & ~31;
     const size_t tile0 = (size_t)rq.part_start + ((size_t)hk * nch + c) * M32 + (size_t)(cg * COLS + ct * 32);
     uint16_t* dst = a.part_o + tile0 * D;
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;  // 0: no key of this chunk is visible to the column
-    for (int dt = 0; dt < DT; ++dt)
-      for (int j = 0; j < 2; ++j) {
-        u32x4 w;
-        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(acc[dt][8 * j + 2 * e] * inv, acc[dt][8 * j + 2 * e + 1] * inv);
-        *(u32x4*)(dst + ((dt * 2 + j) * 64 + lane) * 8) = w;
+    if (valid) {
+      for (int dt = 0; dt < DT; ++dt)
+        for (int j = 0; j < 2; ++j) {
+          u32x4 w;
+          for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(acc[dt][8 * j + 2 * e] * inv, acc[dt][8 * j + 2 * e + 1] * inv);
+          uint16_t* at = dst + ((dt * 2 + j) * 64 + lane) * 8;
+          if constexpr (PERSIST) store16_coherent(at, w);
+          else *(u32x4*)at = w;
+        }
+      if (lh == 0) {
+        if constexpr (PERSIST) store8_coherent(a.part_ml + 2 * (tile0 + lc), m_run, l_tot);
+        else *(float2*)(a.part_ml + 2 * (tile0 + lc)) = make_float2(m_run, l_tot);
       }
-    if (lh == 0) *(float2*)(a.part_ml + 2 * (tile0 + lc)) = make_float2(m_run, l_tot);
+    }
+    if constexpr (PERSIST) {
+      wait_vmcnt<0>();
+      if (lane == 0)
+        __hip_atomic_fetch_add(a.sync + kSyncHeader + rq.comb_start + hk * ncg + cg, 1, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 }
 
 // Merge of the split-KV partials.  Work item = (request, KV head, 32-column
-// tile, slice of 128 16-byte rows of the tile's fragment-ordered block).  A
+// tile, slice of ROWS 16-byte rows of the tile's fragment-ordered block).  A
 // row (8 head dims of one column: two runs of 4) is merged by PARTS threads:
 // part j takes chunks j, j + PARTS, ... -- up to eight chunks' loads in
 // flight at a time -- and merges them with online rescaling (chunk weight
 // exp(m_c - m) * l_c on the chunk's normalised output); the parts' states
-// then meet in LDS and part 0 merges them in order and writes 8 bf16
-// outputs.  PARTS is 4 when some request of the launch has more than 8
-// chunks and the grid is small (up to 32 chunks then cost one memory round
-// trip on a latency-bound launch), else 1.
-constexpr int kCombRows = 128;  // 16-byte rows per work item
+// then meet in LDS (`st`, (PARTS - 1) x 10 x ROWS floats) and part 0 merges
+// them in order and writes 8 bf16 outputs.
+//
+// PERSIST: the item is a combine item of the one-launch kernel.  Thread 0
+// first waits until every tile of every chunk of the item's column group has
+// been counted finished (all of those main items were taken from the queue
+// before any combine item, by running work groups, so the wait ends; a
+// bounded spin sets the error word instead of hanging if it ever did not),
+// and the partials are read device-coherently.  The last combine item of a
+// column group to pass the wait returns its two counters to zero for the
+// next call.
+constexpr int kCombRows = 128;         // 16-byte rows per item of the combine kernel
+constexpr int kCombRowsPersist = 256;  // ... and of a combine item of the one-launch kernel
+constexpr int kCombPartsPersist = 3;   // 3 x 256 threads = the one-launch work group
+constexpr int kSpinLimit = 1 << 20;    // polls (each a device round trip, 1-2 us) before giving up
 
-template <int D, int PARTS, typename Plan>
-__global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArgs a, Plan p) {
-  constexpr int SLICES = 4 * D / kCombRows;  // 16-byte rows per tile block / rows per item
-  __shared__ float st[PARTS > 1 ? PARTS - 1 : 1][10][kCombRows];  // parts 1.. : (m, l, o[8]) per row
-  const int item = xcd_item(p.grid_comb);
-  if (item >= p.total_comb) return;
+template <int D, int PARTS, int ROWS, bool PERSIST, typename Plan>
+__device__ __forceinline__ void combine_item(const AttnArgs& a, const Plan& p, const int item, float* st) {
+  constexpr int SLICES = 4 * D / ROWS;  // 16-byte rows per tile block / rows per item
+  static_assert(SLICES >= 1 && 4 * D % ROWS == 0 && ROWS % 64 == 0, "slices of whole waves");
   const int r = find_request(p, item, true);
   const auto rq = p.req[r];
   const int n = rq.nv & 0xffff, L = rq.ctx, T = L + n;
@@ -572,11 +630,37 @@ __global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArg
   const int tiles = M32 / 32;
   const int tile = local % tiles;
   const int hk = local / tiles;
-  const int t = (int)threadIdx.x % kCombRows;
-  const int part = __builtin_amdgcn_readfirstlane((int)threadIdx.x / kCombRows);
-  const int f = slice * kCombRows + t;  // row of the block
+  const int t = (int)threadIdx.x % ROWS;
+  const int part = __builtin_amdgcn_readfirstlane((int)threadIdx.x / ROWS);
+  const int f = slice * ROWS + t;  // row of the block
   const int lane = f & 63, lc = lane & 31, lh = lane >> 5, q = f >> 6;
   const size_t base = (size_t)rq.part_start + (size_t)hk * nch * M32 + (size_t)tile * 32;
+
+  if constexpr (PERSIST) {
+    constexpr int TPG = 256 / 32;  // tiles per column group
+    const int cg = tile / TPG, ncg = (M + 255) / 256;
+    const int nct = min(TPG, tiles - cg * TPG);
+    int32_t* done = a.sync + kSyncHeader + rq.comb_start + hk * ncg + cg;
+    if (threadIdx.x == 0) {
+      const int target = nch * nct;
+      for (int spin = 0; __hip_atomic_load(done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target; ++spin) {
+        // give up after the bound, or (checked every 256 polls) once any wait of this call has
+        if (spin >= kSpinLimit ||
+            ((spin & 255) == 255 && __hip_atomic_load(a.sync + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)) {
+          __hip_atomic_store(a.sync + 2, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(8);
+      }
+      int32_t* started = done + kMaxSyncComb;
+      if (__hip_atomic_fetch_add(started, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nct * SLICES - 1) {
+        __hip_atomic_store(done, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(started, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    lds_barrier();
+    asm volatile("" ::: "memory");  // the partial loads stay after the wait
+  }
 
   float m = kNegInf, l = 0.f;
   float o[8];
@@ -600,8 +684,13 @@ __global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArg
       const int c = c0 + u * PARTS;
       if (c < nch) {
         const size_t t0 = base + (size_t)c * M32;
-        ml[u] = *(const float2*)(a.part_ml + 2 * (t0 + lc));
-        v[u] = *(const u32x4*)(a.part_o + t0 * D + (size_t)f * 8);
+        if constexpr (PERSIST) {
+          ml[u] = load8_coherent(a.part_ml + 2 * (t0 + lc));
+          v[u] = load16_coherent(a.part_o + t0 * D + (size_t)f * 8);
+        } else {
+          ml[u] = *(const float2*)(a.part_ml + 2 * (t0 + lc));
+          v[u] = *(const u32x4*)(a.part_o + t0 * D + (size_t)f * 8);
+        }
       }
     }
 #pragma unroll
@@ -619,26 +708,26 @@ __global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArg
   }
   // Parts 1.. hand (m, l, normalised o) to part 0.
   if (PARTS > 1 && part > 0) {
-    float* s = &st[part - 1][0][t];
+    float* s = st + ((part - 1) * 10) * ROWS + t;
     s[0] = m;
-    s[kCombRows] = l;
+    s[ROWS] = l;
     const float inv = l > 0.f ? 1.f / l : 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) s[(2 + e) * kCombRows] = o[e] * inv;
+    for (int e = 0; e < 8; ++e) s[(2 + e) * ROWS] = o[e] * inv;
   }
   if (PARTS > 1) {
-    __syncthreads();
+    lds_barrier();
     if (part > 0) return;
   }
 #pragma unroll
   for (int j = 0; j < PARTS - 1; ++j) {
-    const float* s = &st[j][0][t];
+    const float* s = st + (j * 10) * ROWS + t;
     const float mj = s[0];
     if (mj == kNegInf) continue;
     float oc[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) oc[e] = s[(2 + e) * kCombRows];
-    absorb(mj, s[kCombRows], oc);
+    for (int e = 0; e < 8; ++e) oc[e] = s[(2 + e) * ROWS];
+    absorb(mj, s[ROWS], oc);
   }
   const int gc = tile * 32 + lc;
   if (gc >= M) return;
@@ -657,8 +746,88 @@ __global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArg
   if (a.lse != nullptr && f < 32) a.lse[orow] = m * a.sm_scale + __logf(l);
 }
 
+// Main kernel of the two-launch mode: one work item per work group, in
+// dispatch order.  One request: its heads' chunk ranges go to one XCD each
+// (shared q and page list in that XCD's L2).  Several: dispatch order, so the
+// longest requests, which come first, spread over all XCDs.
+template <int D, typename Plan>
+__global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, Plan p) {
+  __shared__ __attribute__((aligned(16))) uint16_t lds[(kKBufs + kVBufs) * kSuper * D];
+  const int item = p.num_req == 1 ? xcd_item(p.grid_items) : (int)blockIdx.x;
+  if (item >= p.total_items) return;
+  attn_item<D, Plan, false>(a, p, item, lds);
+}
+
+template <int D, int PARTS, typename Plan>
+__global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArgs a, Plan p) {
+  __shared__ float st[(PARTS > 1 ? PARTS - 1 : 1) * 10 * kCombRows];
+  const int item = xcd_item(p.grid_comb);
+  if (item >= p.total_comb) return;
+  combine_item<D, PARTS, kCombRows, false>(a, p, item, st);
+}
+
+// One-launch work-queue kernel (launches with split requests).  The queue
+// is every main item (longest request first), then every combine item.  A
+// work group takes its first item by its index (as the dispatcher would) and
+// each further one from an atomic queue head; it asks for the next item at
+// the start of the current one, so the request's latency is hidden.  The
+// combine items of a request run in the same launch, as soon as its chunks
+// are done, on work groups that would otherwise sit idle or exit: no second
+// launch, and no kernel boundary between a split request's chunks and their
+// merge.  The last work group to leave returns the queue head and the exit
+// count to zero for the next call.
+template <int D, typename Plan>
+__global__ __launch_bounds__(kThreads) void attn_persist_kernel(AttnArgs a, Plan p) {
+  constexpr int WORDS = (kKBufs + kVBufs) * kSuper * D / 2;  // 32-bit words of LDS (all of it)
+  __shared__ __attribute__((aligned(16))) uint16_t lds[(kKBufs + kVBufs) * kSuper * D];
+  // The next item's index passes through the last word of the second V
+  // buffer: no key-group merge area or combine exchange reaches it, and the
+  // next item's first copies (K and V of buffer 0, K of buffer 1) do not
+  // write it before its first barrier.
+  int* const s_next = reinterpret_cast<int*>(lds) + WORDS - 1;
+  static_assert(kCombRowsPersist * kCombPartsPersist == kThreads, "combine items use the whole work group");
+  static_assert((kCombPartsPersist - 1) * 10 * kCombRowsPersist < WORDS - 1, "combine exchange below the slot");
+  static_assert(kWaves * (64 * 16 * (D / 32) + 128) < WORDS - 1, "key-group merge area below the slot");
+  const int total = p.total_items + p.total_comb;
+  const int grid = p.persist_grid;
+  // First item: the work group's index, which the queue head then continues
+  // from.  When every main item is in this first round, one request's items
+  // are dealt as the main kernel deals them (a head's chunks to one XCD): a
+  // permutation of [0, grid_items), the combine items after it unchanged.
+  int item = (int)blockIdx.x;
+  if (p.num_req == 1 && p.grid_items <= grid && item < p.grid_items) item = xcd_item(p.grid_items);
+  // When every item is in the first round there is no queue: each work group
+  // runs its one item and leaves, with no queue atomics on its way out.
+  const bool queued = total > grid;
+  while ((unsigned)item < (unsigned)total) {  // (also stops on a queue head that was not zero)
+    int nxt = total;
+    if (queued && threadIdx.x == 0)
+      nxt = grid + __hip_atomic_fetch_add(a.sync, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (item < p.total_items)
+      attn_item<D, Plan, true>(a, p, item, lds);
+    else
+      combine_item<D, kCombPartsPersist, kCombRowsPersist, true>(a, p, item - p.total_items,
+                                                                reinterpret_cast<float*>(lds));
+    if (!queued) break;
+    lds_barrier();  // every wave is done with LDS
+    if (threadIdx.x == 0) *s_next = nxt;
+    lds_barrier();
+    item = *s_next;
+  }
+  if (queued && threadIdx.x == 0 &&
+      __hip_atomic_fetch_add(a.sync + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (int)gridDim.x - 1) {
+    __hip_atomic_store(a.sync, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(a.sync + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
 template <int D, typename Plan>
 hipError_t launch_impl(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
+  if (plan.persist_grid > 0) {
+    hipLaunchKernelGGL((attn_persist_kernel<D, Plan>), dim3(plan.persist_grid), dim3(kThreads), 0, stream, args,
+                       plan);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL((attn_fwd_kernel<D, Plan>), dim3(plan.grid_items), dim3(kThreads), 0, stream, args, plan);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -13,6 +13,14 @@ constexpr int kPageSize = 16;
 constexpr int kMaxReqPerLaunch = 128;  // equals RG_ATTN_MAX_REQS_PER_LAUNCH
 constexpr int kKeyTile = 128;          // keys per LDS buffer; chunks are multiples of it
 constexpr int kMaxChunkKeys = 1 << 16;  // keys per work item at most
+constexpr int kSyncHeader = 4;          // queue head, exit count, error flag, pad
+// Combine items of one launch the one-launch kernel can count (two counters
+// each); launches with more use the main kernel plus the combine kernel.
+constexpr int kMaxSyncComb = 16384;
+// The synchronisation words open every attention workspace at a fixed place
+// and size, so calls with different layouts can share a workspace: the words
+// one call leaves at zero are never another call's partials.
+constexpr int kSyncWords = kSyncHeader + 2 * kMaxSyncComb;
 
 // Per-request data of one attention launch.  Everything a work group needs
 // about its request travels in the kernel arguments, so no table has to be
@@ -52,6 +60,8 @@ struct AttnPlanT {
   int32_t grid_comb;       // total_comb rounded up to a multiple of 8
   int32_t cols_per_group;  // query columns one work group covers (256)
   int32_t max_chunks;      // most chunks of one split request (picks the combine variant)
+  int32_t persist_grid;    // 0: main kernel + combine kernel; else the work groups of the
+                           // one-launch work-queue kernel (main items, then combine items)
   Req req[MaxReq + 1];     // entry num_req holds the end sentinels
 };
 using AttnPlan = AttnPlanT<AttnReq, kMaxReqPerLaunch>;
@@ -68,6 +78,9 @@ struct AttnArgs {
   const int32_t* page_indices;
   uint16_t* part_o;  // per 32-column tile: 32 x D bf16 normalised partial outputs, MFMA fragment order
   float* part_ml;  // [partial columns][2] fp32 (running max of raw scores, sum)
+  int32_t* sync;   // kSyncWords words, zero between calls: queue head, exit count, error
+                   // flag, pad, then finished-tile counts (indexed by a column group's
+                   // first combine item) and, kMaxSyncComb words on, started-combine counts
   int32_t hq, hkv, g;
   float sm_scale;    // natural-log domain scale
   float scale_log2;   // sm_scale * log2(e)

@@ -244,6 +244,32 @@ def test_plan_chunk_override_and_workspace_monotone(monkeypatch):
     assert sizes == sorted(sizes)
 
 
+@pytest.mark.parametrize("persist", ["1", "0"])
+@pytest.mark.parametrize("name", ["low", "mid", "high"])
+def test_plan_one_launch_mode_and_sync_words(monkeypatch, persist, name):
+    """Launches with a split request run as one work-queue launch unless
+    RG_ATTN_PERSIST=0; the synchronisation words (queue head, exit count,
+    error word, then two counters per merge item) sit after the partials."""
+    monkeypatch.setenv("RG_ATTN_PERSIST", persist)
+    lay = W.make_layout(name, seed=1)
+    s = lay.spec
+    info = _plan(_L(R=lay.num_requests, hq=s.num_q_heads, hkv=s.num_kv_heads, D=s.head_dim,
+                    num_pages=lay.num_pages, ctx=lay.ctx_len, nv=lay.n_verify, n=lay.q_len,
+                    pages=np.diff(lay.page_indptr)))
+    if info.split_requests == 0:
+        assert info.persistent_launches == 0 and info.sync_offset == -1 and info.workspace_bytes == 0
+        assert info.sync_words == 0
+        return
+    assert info.persistent_launches == (info.num_launches if persist == "1" else 0)
+    g = s.num_q_heads // s.num_kv_heads
+    tiles = sum(s.num_kv_heads * -(-int(lay.q_len[r]) * g // 32)
+                for r in range(lay.num_requests) if -(-int(lay.kv_len[r]) // info.chunk_keys) > 1)
+    merge_items = tiles * (4 * s.head_dim // (256 if persist == "1" else 128))
+    # fixed place and size whatever the layout, room for every merge item's two counters
+    assert info.sync_offset == 0 and info.sync_words == 4 + 2 * 16384 >= 4 + 2 * merge_items
+    assert info.workspace_bytes >= (4 * info.sync_words + info.partial_columns * (s.head_dim * 2 + 8))
+
+
 def test_generators_are_deterministic():
     a = W.make_layout("high", seed=5)
     b = W.make_layout("high", seed=5)

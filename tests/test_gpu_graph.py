@@ -21,7 +21,7 @@ def test_graph_replays_match_eager(fused):
     rp = torch.as_tensor(lay.row_indptr, device=DEV)
     layout = binding.make_layout(inp["q"], inp["k_cache"], lay.q_indptr, lay.n_verify, lay.ctx_len,
                                  lay.page_indptr, page_idx)
-    ws = torch.empty(max(16, binding.attention_workspace_bytes(layout)), dtype=torch.uint8, device=DEV)
+    ws = binding.new_workspace(binding.attention_workspace_bytes(layout), DEV)
     vws = binding.new_workspace(binding.verify_accept_workspace_bytes(
         lay.num_requests, lay.total_verify_rows, lay.spec.vocab), DEV)
     dws = binding.new_workspace(binding.draft_confidence_workspace_bytes(lay.total_draft_rows, lay.spec.vocab), DEV)
