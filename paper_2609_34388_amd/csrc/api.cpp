@@ -142,23 +142,27 @@ int device_cus() {
 // lookup, page numbers, first copies, epilogue: several microseconds) besides
 // its keys, and splitting a request adds partial outputs and the combine
 // kernel; items are dispatched longest request first, so with a couple of
-// items per CU the dispatcher balances them.  `pair_keys` holds T of every
-// (request, KV head, column group); with S = sum / 256 (one CU's share): the
-// longest chunk (a multiple of the LDS buffer, at least 256 keys, at most S)
-// that still gives at least two items per CU -- no split at all when the
-// pairs alone do and none exceeds S.  Measured against the earlier rule
-// (chunks within S / 4, three pairs per CU before a request stays whole):
-// `long` 1368 -> 1340 us (whole requests), `mid` 103 -> 100 us.  Uneven
-// splits are what hurt: at `long`, 24576-key chunks (a full chunk plus a
-// short remainder per request) took 1633 us.
-int choose_chunk(const std::vector<int64_t>& pair_keys) {
+// items per CU the dispatcher balances them.  With S = all keys / 256 (one
+// CU's share): the longest chunk (a multiple of the LDS buffer, at least 256
+// keys, at most S) that still gives at least two items per CU -- so a
+// request stays whole when the pairs alone give two items per CU and none
+// exceeds S.  `pair_keys` holds T of every (request, column group); each
+// stands for Hkv pairs, one per KV head.  Measured against the earlier rule (chunks within S / 4, three
+// pairs per CU before a request stays whole): `long` 1368 -> 1340 us (whole
+// requests; 3072-12288-key chunks measured 1362-1398 us), `mid` 103 -> 100
+// us.  Uneven splits are what hurt: at `long`, 24576-key chunks (a full chunk
+// plus a short remainder per request) took 1633 us.  A dispatch simulation
+// choosing shorter chunks to fill the last round of items helped on two of
+// five `mid` draws and lost up to 11 % on the others: per-item costs beyond
+// the keys are larger and less regular than a fixed start-up.
+int choose_chunk(const std::vector<int64_t>& pair_keys, int hkv) {
   const int forced = env_int("RG_ATTN_CHUNK", 0);
   if (forced > 0) return (int)std::min<int64_t>(kMaxChunkKeys, round_up(forced, kKeyTile));
   constexpr int64_t kCUs = 256;
   const int64_t floor_keys = round_up(std::max(kKeyTile, env_int("RG_ATTN_MIN_CHUNK", 256)), kKeyTile);
   int64_t total = 0, longest = 0;
   for (int64_t t : pair_keys) {
-    total += t;
+    total += t * hkv;
     longest = std::max(longest, t);
   }
   const int64_t share = total / kCUs;
@@ -166,7 +170,7 @@ int choose_chunk(const std::vector<int64_t>& pair_keys) {
   auto items = [&](int64_t chunk) {
     int64_t n = 0;
     for (int64_t t : pair_keys) n += (t + chunk - 1) / chunk;
-    return n;
+    return n * hkv;
   };
   int64_t hi = std::min(whole, std::max(floor_keys, round_up(share, kKeyTile)));
   int64_t lo = floor_keys;
@@ -199,14 +203,14 @@ rg_status plan_attention(const rg_attn_layout* L, const rg_branch_layout* B, Ful
   const int g = L->num_q_heads / L->num_kv_heads;
   const int hkv = L->num_kv_heads;
   fp.cols_per_group = 256;  // 8 waves x 32 columns per work group
-  std::vector<int64_t> pair_keys;
+  std::vector<int64_t> pair_keys;  // one entry per (request, column group): Hkv pairs each
   for (int r = 0; r < R; ++r) {
     const int64_t n = L->q_indptr[r + 1] - L->q_indptr[r];
     if (n == 0) continue;
     const int64_t ncg = (n * g + fp.cols_per_group - 1) / fp.cols_per_group;
-    for (int64_t k = 0; k < hkv * ncg; ++k) pair_keys.push_back((int64_t)L->ctx_len[r] + n);
+    for (int64_t cg = 0; cg < ncg; ++cg) pair_keys.push_back((int64_t)L->ctx_len[r] + n);
   }
-  fp.chunk = choose_chunk(pair_keys);
+  fp.chunk = choose_chunk(pair_keys, hkv);
   // Longest requests first: work groups are dispatched in item order, so the
   // long items start early and the short ones fill in at the end.
   std::vector<int> order(R);
