@@ -91,6 +91,10 @@ __device__ __forceinline__ void load_chunk(const uint16_t* row, int v0, int v1, 
 #pragma unroll
     for (int u = 0; u < kU; ++u)
       w[u] = __builtin_nontemporal_load((const u32x4*)(row + v0 + (u * kLogitThreads + tid) * 8));
+    // All loads go out before the first use of any: otherwise the scheduler
+    // may convert the first load's entries before issuing the others, and the
+    // wait for that load costs a second memory round trip.
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < kU; ++u) widen8(w[u], x + 8 * u);
     return;
