@@ -139,11 +139,12 @@ def test_empty_requests_and_workspace_reuse():
         assert torch.equal(a[k], b[k]), k
 
 
-@pytest.mark.parametrize("rows,reqs", [(16, 9), (17, 9), (16, 1), (40, 300)])
+@pytest.mark.parametrize("rows,reqs", [(16, 9), (17, 9), (16, 1), (40, 300), (16, 200), (8, 255), (8, 256)])
 def test_finalize_group_layouts(rows, reqs):
     """Requests of many sizes (empty ones among them, more requests than a
     work group has threads) over a 16-chunk vocabulary give the oracle's
-    accept lengths, next tokens and e_t."""
+    accept lengths, next tokens and e_t (200 to 256 requests over 8 or 16
+    rows: mostly empty requests, every one finalised)."""
     vocab = 128250  # 16 chunks of 8192 entries: 16 lanes per row
     g = torch.Generator(device=DEV).manual_seed(rows * 1000 + reqs)
     logits = (torch.randn(rows, vocab, generator=g, device=DEV) * 2).to(torch.bfloat16)
