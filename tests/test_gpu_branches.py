@@ -107,6 +107,19 @@ def test_multibranch_attention_matches_oracle(name):
     _check(out, lse, _reference(lay, inp, branches))
 
 
+@pytest.mark.parametrize("name", ["overlap", "split", "gap", "quadratic"])
+def test_multibranch_one_launch_mode_matches_oracle(monkeypatch, name):
+    """The branched plans in the one-launch work-queue mode (RG_ATTN_PERSIST=1),
+    every request split over 128-key chunks, against the oracle."""
+    monkeypatch.setenv("RG_ATTN_PERSIST", "1")
+    monkeypatch.setenv("RG_ATTN_CHUNK", "128")
+    ctx, nv, branches = CASES[name]
+    lay = _layout(ctx, nv, branches, seed=len(name) + 40)
+    inp = W.make_attention_inputs(lay, DEV, poison=float("nan"))
+    out, lse = _run(lay, inp, branches)
+    _check(out, lse, _reference(lay, inp, branches))
+
+
 def test_no_branches_is_the_fused_step_bit_for_bit():
     ctx, nv = [300, 57, 1000], [8, 4, 16]
     branches = [[(nv[0], 0, 11)], [], []]
