@@ -379,6 +379,43 @@ def cpu_baseline(lay, inputs, budget_s: float):
     return t_total / runs, runs, blas_threads, len(os.sched_getaffinity(0))
 
 
+def cpu_baseline_rows(lay, budget_s: float):
+    """The oracle beside the rows built past the step, on the same workload:
+    the overlap round's multi-branch attention (request by request, within
+    ``budget_s``; inputs of the same shapes drawn on the host) and one
+    block-sizing round for every request."""
+    import numpy as np
+
+    import oracle
+    from paper_2609_34388_amd import workloads as W
+
+    branches = W.overlap_branches(lay)
+    ov = W.make_overlap_layout(lay, branches)
+    host = W.make_attention_inputs(ov, "cpu")
+    q, k, v = (W.bf16_bits(host[n]) for n in ("q", "k_cache", "v_cache"))
+    done, t_total = 0, 0.0
+    for r in range(ov.num_requests):
+        t0 = time.perf_counter()
+        oracle.oracle_branch_attention(q, k, v, ov.q_indptr, ov.n_verify, ov.ctx_len, ov.page_indptr,
+                                       ov.page_indices, branches, requests=[r])
+        t_total += time.perf_counter() - t0
+        done += 1
+        if t_total >= budget_s:
+            break
+    overlap = {"us_per_request": round(t_total / done * 1e6, 1), "requests_timed": done,
+               "us_all_requests_estimated": round(t_total / done * ov.num_requests * 1e6, 1),
+               "sample": f"{done} of {ov.num_requests} request(s) of the overlap round (verify rows and three "
+                         f"branches each), fp64 numpy oracle"}
+    d = W.make_block_policy_inputs(seed=lay.seed, num_requests=lay.num_requests)
+    cost = [1.0] * len(d["candidates"])
+    t0 = time.perf_counter()
+    oracle.oracle_plan_block_sizes(d["accept_len"], d["accept_entropy"], d["prev_block"], d["entropy_hist"],
+                                   d["candidates"], d["s_edges"], d["value"], cost, 0.5)
+    plan_us = (time.perf_counter() - t0) * 1e6
+    sizing = {"us": round(plan_us, 1), "sample": f"one round for all {lay.num_requests} request(s), oracle"}
+    return {"overlap_multibranch_attention": overlap, "plan_block_sizes": sizing}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -583,6 +620,8 @@ def main(argv=None):
                                   "ms_per_step": round(sec * 1e3, 2), "visible_cores": cores,
                                   "sample": f"{runs} whole step(s) of the same workload (all requests, heads "
                                             f"and rows), fp64 numpy oracle, mean time per step"}
+        if not args.no_overlap or not args.no_block_sizing:
+            result["cpu_baseline"]["beside_next_rows"] = cpu_baseline_rows(lay, min(4.0, args.cpu_budget / 3))
     print(json.dumps(result), flush=True)
     return 0
 
