@@ -14,9 +14,10 @@
 // compute waves of a work group split the group into 32-column tiles and,
 // when there are fewer than 8 tiles, the chunk's 32-key sub-tiles into key
 // groups; 4 more waves only issue the copies into LDS.
-// Requests whose keys span several chunks write un-normalised partial outputs
+// Requests whose keys span several chunks write normalised partial outputs
 // plus (max, sum) per column; a second kernel merges them with the usual
-// log-sum-exp weights.
+// log-sum-exp weights (or, in the opt-in one-launch mode, merge items of the
+// same launch, taken from a work queue once the chunks they merge are done).
 //
 // K and V of 128 keys (8 pages) at a time are copied straight into LDS
 // (three K buffers and two V buffers: the next buffer's copies, and with
@@ -329,9 +330,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
 #pragma unroll
     for (int j = 0; j < kSuper / kPageSize; ++j) pg[j] = chunk_pages[min(base + j, npg - 1)];
   };
-  auto issue_k = [&](int s) {
-    int pg[kSuper / kPageSize];
-    read_pages(s, pg);
+  auto issue_k = [&](int s, const int (&pg)[kSuper / kPageSize]) {
 #pragma unroll
     for (int i = 0; i < GP / 2; ++i) {
       const int b = pw + i * kProducers;  // wave-uniform
@@ -341,9 +340,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
               (uint32_t)(uintptr_t)(kbuf(s) + b * 512));
     }
   };
-  auto issue_v = [&](int s) {
-    int pg[kSuper / kPageSize];
-    read_pages(s, pg);
+  auto issue_v = [&](int s, const int (&pg)[kSuper / kPageSize]) {
 #pragma unroll
     for (int i = 0; i < GP / 2; ++i) {
       const int b = pw + i * kProducers;  // V block of the buffer
@@ -460,22 +457,38 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
     // pace): K runs two buffers ahead.  Issue order K(0), V(0), K(1); then at
     // buffer s: V(s + 1), K(s + 2), so when V(s) is complete only K(s + 1) can
     // still be out.  Otherwise K and V of s + 1 go out together at buffer s.
+    // The page numbers a buffer's copies need are read before the barrier
+    // that frees its LDS, so their load latency passes while the buffer
+    // being computed is still in use, not after it.
     const bool deep = nct <= 4;  // every tile split over key groups
-    issue_k(0);
-    issue_v(0);
-    if (deep && nsup > 1) issue_k(1);
+    int pa[kSuper / kPageSize], pb[kSuper / kPageSize];
+    read_pages(0, pa);
+    issue_k(0, pa);
+    issue_v(0, pa);
+    if (deep && nsup > 1) {
+      read_pages(1, pb);
+      issue_k(1, pb);
+    }
     for (int s = 0; s < nsup; ++s) {
+      // deep: V(s + 1) uses the pages of s + 1 (still in pb), K(s + 2) those of s + 2
+      if (deep) {
+        if (s + 2 < nsup) read_pages(s + 2, pa);
+      } else if (s + 1 < nsup) {
+        read_pages(s + 1, pa);
+      }
       if (deep && s + 1 < nsup) wait_vmcnt<GP / 2>();  // this copy wave's K(s) and V(s)
       else wait_vmcnt<0>();
       lds_barrier();  // everyone's copies of buffer s are in; buffers of s - 1 are no longer read
       const int nvalid = kend - (kbeg + s * kSuper);
       if (nvalid < kSuper) tail_fixup(s, nvalid);
       if (deep) {
-        if (s + 1 < nsup) issue_v(s + 1);  // into the V buffer of s - 1
-        if (s + 2 < nsup) issue_k(s + 2);  // into the K buffer of s - 1
+        if (s + 1 < nsup) issue_v(s + 1, pb);  // into the V buffer of s - 1
+        if (s + 2 < nsup) issue_k(s + 2, pa);  // into the K buffer of s - 1
+#pragma unroll
+        for (int j = 0; j < kSuper / kPageSize; ++j) pb[j] = pa[j];
       } else if (s + 1 < nsup) {
-        issue_k(s + 1);  // into the K buffer of s - 2
-        issue_v(s + 1);  // into the V buffer of s - 1
+        issue_k(s + 1, pa);  // into the K buffer of s - 2
+        issue_v(s + 1, pa);  // into the V buffer of s - 1
       }
     }
     if constexpr (PERSIST) {
