@@ -147,7 +147,7 @@ rg_status rg_draft_verify_attention_workspace(const rg_attn_layout* layout, size
  * instead as one work-queue launch (the library's variant of mapping mixed
  * ragged attention work onto the compute units, Sec. 5.3): at most one work
  * group per compute unit takes the work items (request, KV head, column
- * group, chunk; longest request first) and then the merge items from an
+ * group, chunk; costliest request first) and then the merge items from an
  * atomic queue, and a merge item starts as soon as the chunks it merges are
  * done.  It gives the same results within rounding and measured slower on
  * MI355X.  The workspace opens with the queue and per-merge counters, at the

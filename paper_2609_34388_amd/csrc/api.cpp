@@ -141,7 +141,7 @@ int device_cus() {
 // Keys per work item.  An item costs a fixed start-up and wind-down (request
 // lookup, page numbers, first copies, epilogue: several microseconds) besides
 // its keys, and splitting a request adds partial outputs and the combine
-// kernel; items are dispatched longest request first, so with a couple of
+// kernel; items are dispatched costliest request first, so with a couple of
 // items per CU the dispatcher balances them.  With S = all keys / 256 (one
 // CU's share): the longest chunk (a multiple of the LDS buffer, at least 256
 // keys, at most S) that still gives at least two items per CU -- so a

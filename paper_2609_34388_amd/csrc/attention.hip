@@ -762,7 +762,7 @@ __device__ __forceinline__ void combine_item(const AttnArgs& a, const Plan& p, c
 // Main kernel of the two-launch mode: one work item per work group, in
 // dispatch order.  One request: its heads' chunk ranges go to one XCD each
 // (shared q and page list in that XCD's L2).  Several: dispatch order, so the
-// longest requests, which come first, spread over all XCDs.
+// costliest requests, which come first, spread over all XCDs.
 template <int D, typename Plan>
 __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(AttnArgs a, Plan p) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[(kKBufs + kVBufs) * kSuper * D];
@@ -780,7 +780,7 @@ __global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArg
 }
 
 // One-launch work-queue kernel (launches with split requests).  The queue
-// is every main item (longest request first), then every combine item.  A
+// is every main item (costliest request first), then every combine item.  A
 // work group takes its first item by its index (as the dispatcher would) and
 // each further one from an atomic queue head; it asks for the next item at
 // the start of the current one, so the request's latency is hidden.  The
