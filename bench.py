@@ -10,6 +10,9 @@ are timed too.  Inputs are
 seeded synthetic tensors resident in HBM before timing starts; several
 copies of every input are rotated through the steps so that the working
 set exceeds the 256 MB Infinity Cache and the numbers are HBM numbers.
+Where one copy of the inputs fits in that cache, ``warm_cache`` reports the
+step, the attention call and the logit round with one copy reused by every
+call, labelled as such (context only).
 
 Prints one JSON line.  ``value`` is the step's achieved fraction of the HBM
 roofline (algorithmic bytes of all three calls / step time / 8 TB/s), in
@@ -53,6 +56,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 CACHE_DEFEAT_BYTES = 512 << 20
+WARM_FIT_BYTES = 128 << 20  # one input copy this small stays in the 256 MB Infinity Cache
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_low_traffic.md")
@@ -606,6 +610,19 @@ def main(argv=None):
         result["attention_one_launch"] = {"us": round(one_ms * 1e3, 3),
                                           "persistent_launches": one_plan["persistent_launches"],
                                           "time_vs_two_launches": round(one_ms / attn_ms, 3)}
+    if copies > 1 and per_copy <= WARM_FIT_BYTES:
+        # Labelled warm-cache figures, never the headline: every call of the
+        # graph reuses input copy 0, which then stays in the Infinity Cache.
+        warm_step = time_calls(lambda i: step(0))
+        warm_attn = time_calls(lambda i: attention(0))
+        warm_round = time_calls(lambda i: logit_round(0))
+        result["warm_cache"] = {
+            "note": "inputs resident in the 256 MB Infinity Cache (one input copy reused by every call); "
+                    "context only, the headline numbers above rotate copies past the cache",
+            "input_bytes": per_copy, "ms_per_step": round(warm_step, 5),
+            "attention_us": round(warm_attn * 1e3, 3),
+            "attention_gbps": round(work["attn_bytes"] / (warm_attn * 1e-3) / 1e9, 1),
+            "logit_round_us": round(warm_round * 1e3, 3)}
     if not args.no_overlap:
         result["overlap"] = overlap_leg(lay, dev, args.steps, args.warmup, capture, time_calls,
                                         (vout, dout, torch.as_tensor(lay.draft_row_indptr, device=dev)))
