@@ -372,15 +372,24 @@ def cpu_baseline(lay, inputs, budget_s: float):
     vl, dl = W.bf16_bits(inputs["verify_logits"]), W.bf16_bits(inputs["draft_logits"])
     tok = inputs["draft_tokens"].cpu().numpy()
     runs, t_total = 0, 0.0
+    parts = [0.0, 0.0, 0.0]  # attention, accept, confidence
     while runs == 0 or (t_total < budget_s and runs < 50):
         t0 = time.perf_counter()
         oracle.oracle_attention(q, k, v, lay.q_indptr, lay.n_verify, lay.ctx_len, lay.page_indptr,
                                 lay.page_indices)
+        t1 = time.perf_counter()
         oracle.oracle_accept(vl, lay.row_indptr, tok)
+        t2 = time.perf_counter()
         oracle.oracle_confidence(dl)
-        t_total += time.perf_counter() - t0
+        t3 = time.perf_counter()
+        for j, dt in enumerate((t1 - t0, t2 - t1, t3 - t2)):
+            parts[j] += dt
+        t_total += t3 - t0
         runs += 1
-    return t_total / runs, runs, blas_threads, len(os.sched_getaffinity(0))
+    split = {"oracle_attention_ms": round(parts[0] / runs * 1e3, 2),
+             "oracle_accept_ms": round(parts[1] / runs * 1e3, 2),
+             "oracle_confidence_ms": round(parts[2] / runs * 1e3, 2)}
+    return t_total / runs, runs, blas_threads, len(os.sched_getaffinity(0)), split
 
 
 def cpu_baseline_rows(lay, budget_s: float):
@@ -630,11 +639,11 @@ def main(argv=None):
         result["block_sizing"] = block_sizing_leg(lay, dev, time_calls)
     if not args.no_cpu_baseline:
         host = {k: base[k] for k in ("q", "k_cache", "v_cache", "verify_logits", "draft_logits", "draft_tokens")}
-        sec, runs, threads, cores = cpu_baseline(lay, host, args.cpu_budget)
+        sec, runs, threads, cores, split = cpu_baseline(lay, host, args.cpu_budget)
         cpu_gbps = step_bytes / sec / 1e9
         result["cpu_baseline"] = {"value": round(100.0 * cpu_gbps / HBM_PEAK_GBPS, 6),
                                   "unit": result["unit"], "cores": threads, "kind": "oracle",
-                                  "ms_per_step": round(sec * 1e3, 2), "visible_cores": cores,
+                                  "ms_per_step": round(sec * 1e3, 2), "visible_cores": cores, **split,
                                   "sample": f"{runs} whole step(s) of the same workload (all requests, heads "
                                             f"and rows), fp64 numpy oracle, mean time per step"}
         if not args.no_overlap or not args.no_block_sizing:
