@@ -141,24 +141,27 @@ int device_cus() {
 // Keys per work item.  An item costs a fixed start-up and wind-down (request
 // lookup, page numbers, first copies, epilogue: several microseconds) besides
 // its keys, and splitting a request adds partial outputs and the combine
-// kernel; items are dispatched costliest request first, so with a couple of
-// items per CU the dispatcher balances them.  With S = all keys / 256 (one
-// CU's share): the longest chunk (a multiple of the LDS buffer, at least 256
-// keys, at most S) that still gives at least two items per CU -- so a
-// request stays whole when the pairs alone give two items per CU and none
-// exceeds S.  `pair_keys` holds T of every (request, column group); each
-// stands for Hkv pairs, one per KV head.  Measured against the earlier rule (chunks within S / 4, three
-// pairs per CU before a request stays whole): `long` 1368 -> 1340 us (whole
-// requests; 3072-12288-key chunks measured 1362-1398 us), `mid` 103 -> 100
-// us.  Uneven splits are what hurt: at `long`, 24576-key chunks (a full chunk
-// plus a short remainder per request) took 1633 us.  A dispatch simulation
-// choosing shorter chunks to fill the last round of items helped on two of
-// five `mid` draws and lost up to 11 % on the others: per-item costs beyond
-// the keys are larger and less regular than a fixed start-up.
+// kernel; items are dispatched costliest request first, and one work group
+// fills a CU, so items run in rounds of 256.  The rule: the shortest chunk (a
+// multiple of the LDS buffer, at least 256 keys, at most S = all keys / 256,
+// one CU's share) whose items fit in two rounds -- the finest split that
+// leaves no third round for a few items to run alone; when even chunks of S
+// give more than two rounds, chunks of S (requests no longer than S stay
+// whole).  `pair_keys` holds T of every (request, column group); each stands
+// for Hkv pairs, one per KV head.  Measured on twelve `mid` draws against
+// the earlier rule (the longest chunk still giving two items per CU, which
+// usually left a short third round): -9.2 % on average, from 0 to -15 %
+// (same-host A/B); `tiny`, `low`, `high` and `long` get the same chunks as
+// before.  Earlier
+// measurements behind the bounds: uneven splits hurt most (at `long`,
+// 24576-key chunks, a full chunk plus a short remainder per request, took
+// 1633 us against 1340 us whole), and finer chunks cost more than a dispatch
+// model with a fixed start-up predicts (merge work, partial traffic).
 int choose_chunk(const std::vector<int64_t>& pair_keys, int hkv) {
   const int forced = env_int("RG_ATTN_CHUNK", 0);
   if (forced > 0) return (int)std::min<int64_t>(kMaxChunkKeys, round_up(forced, kKeyTile));
   constexpr int64_t kCUs = 256;
+  constexpr int64_t kTwoRounds = 2 * kCUs;
   const int64_t floor_keys = round_up(std::max(kKeyTile, env_int("RG_ATTN_MIN_CHUNK", 256)), kKeyTile);
   int64_t total = 0, longest = 0;
   for (int64_t t : pair_keys) {
@@ -167,21 +170,22 @@ int choose_chunk(const std::vector<int64_t>& pair_keys, int hkv) {
   }
   const int64_t share = total / kCUs;
   const int64_t whole = std::min<int64_t>(kMaxChunkKeys, std::max(floor_keys, round_up(longest, kKeyTile)));
-  auto items = [&](int64_t chunk) {
+  auto items = [&](int64_t chunk) {  // nonincreasing in chunk
     int64_t n = 0;
     for (int64_t t : pair_keys) n += (t + chunk - 1) / chunk;
     return n * hkv;
   };
-  int64_t hi = std::min(whole, std::max(floor_keys, round_up(share, kKeyTile)));
-  int64_t lo = floor_keys;
-  if (items(lo) < 2 * kCUs) return (int)lo;
-  while (lo < hi) {  // invariant: items(lo) >= 2 * kCUs
-    const int64_t mid = round_up((lo + hi + 1) / 2, kKeyTile);
-    if (mid > hi) break;
-    if (items(mid) >= 2 * kCUs) lo = mid;
-    else hi = mid - kKeyTile;
+  const int64_t hi_keys = std::min(whole, std::max(floor_keys, round_up(share, kKeyTile)));
+  if (items(hi_keys) > kTwoRounds) return (int)hi_keys;
+  if (items(floor_keys) <= kTwoRounds) return (int)floor_keys;
+  // Buffers per chunk: items(lo) > two rounds >= items(hi).
+  int64_t lo = floor_keys / kKeyTile, hi = hi_keys / kKeyTile;
+  while (hi - lo > 1) {
+    const int64_t mid = (lo + hi) / 2;
+    if (items(mid * kKeyTile) <= kTwoRounds) hi = mid;
+    else lo = mid;
   }
-  return (int)lo;
+  return (int)(hi * kKeyTile);
 }
 
 // Branch words of request r (see AttnReqBr); all zero when B is NULL or
