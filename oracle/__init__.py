@@ -29,5 +29,6 @@ from .blocksize import (  # noqa: F401
     oracle_bucket,
     oracle_plan_block_sizes,
     oracle_route,
+    oracle_utilities,
     s_bin,
 )

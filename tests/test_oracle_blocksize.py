@@ -12,7 +12,8 @@ import itertools
 import numpy as np
 import pytest
 
-from oracle import oracle_block_state, oracle_bucket, oracle_plan_block_sizes, oracle_route, s_bin
+from oracle import (oracle_block_state, oracle_bucket, oracle_plan_block_sizes, oracle_route,
+                    oracle_utilities, s_bin)
 
 CAND = [8, 16, 32]
 
@@ -22,9 +23,10 @@ def test_state_closed_form():
     assert s == np.float32(-2.0) and zb == 1 and full == 1
     s, zb, full = oracle_block_state(0.25, 0.5, 32, 7, CAND)
     assert s == np.float32(-0.375) and zb == 2 and full == 0
-    # the sum is rounded to float32 before halving
+    # the definition's real-number mean: the sum is not rounded to float32
+    # (in float32 1 + 2^-24 rounds to 1 and s would be -0.5)
     s, _, _ = oracle_block_state(np.float32(1.0), np.float32(2.0 ** -24), 8, 0, CAND)
-    assert s == np.float32(-0.5)
+    assert s == -(0.5 + 2.0 ** -25)
 
 
 @pytest.mark.parametrize("prev,want", [(8, 0), (12, 0), (16, 1), (31, 1), (32, 2), (64, 2), (4, 0), (0, 0)])
@@ -61,6 +63,34 @@ def test_route_argmax_and_cost():
     assert oracle_route(np.float32(0), 0, 0, CAND, [], v, cost, 1.5) == 16
     # rho 0: the value alone decides
     assert oracle_route(np.float32(0), 0, 0, CAND, [], v, cost, 0.0) == 32
+
+
+def test_route_decides_by_the_real_number_utilities():
+    """Eq. 3's argmax is taken over the utilities as real numbers.  Here
+    rho * cost = fp32(0.3) * 10 = 3 + 2^-23 exactly, so candidate 16 has
+    utility 4 - 3 - 2^-23 = 1 - 2^-23, below candidate 8's 1 - 2^-24: the
+    definition picks 8.  Evaluated in float32 the product rounds (a tie at
+    half an ulp, to even) to 3, candidate 16 gets 1 > 1 - 2^-24 and wins --
+    the kind of mistake a float32 oracle would make."""
+    rho = np.float32(0.3)
+    assert float(rho) * 10 == 3 + 2.0 ** -23 and np.float32(rho * np.float32(10)) == np.float32(3)
+    v = _table([1 - 2.0 ** -24, 4.0, -100.0])
+    cost = [0.0, 10.0, 0.0]
+    assert oracle_route(0.0, 0, 0, CAND, [], v, cost, rho) == 8
+    k, u = oracle_utilities(0.0, 0, 0, CAND, [], v, cost, rho)
+    assert k == 0 and u[0] == 1 - 2.0 ** -24 and u[1] == 1 - 2.0 ** -23 and u[2] == -100.0
+
+
+def test_bin_edges_are_compared_exactly():
+    # s = -(e1 + e2) / 2 lands exactly on an edge: the bin at or above it
+    s, _, _ = oracle_block_state(np.float32(1.5), np.float32(0.5), 8, 0, CAND)
+    assert s == -1.0 and s_bin(s, [-1.0, -0.5]) == 1
+    # 2^-25 below the edge (in float32, 1.5 + (0.5 + 2^-24) rounds to 2 and s
+    # would land on the edge): the bin below
+    e2 = np.float32(0.5 + 2.0 ** -24)
+    assert float(e2) == 0.5 + 2.0 ** -24 and np.float32(np.float32(1.5) + e2) == np.float32(2.0)
+    s, _, _ = oracle_block_state(np.float32(1.5), e2, 8, 0, CAND)
+    assert s == -1.0 - 2.0 ** -25 and s_bin(s, [-1.0, -0.5]) == 0
 
 
 def test_route_reads_the_right_cell():
