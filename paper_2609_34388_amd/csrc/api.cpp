@@ -126,8 +126,10 @@ struct FullPlanT {
   size_t sync_offset = 0;
 };
 
-// Compute units of the current device (the one-launch kernel's work groups,
-// one per CU); 256 (MI355X) when the runtime cannot say.
+// Compute units of the current device: the rounds of the chunk rule and the
+// one-launch kernel's work groups (one per CU); 256 (MI355X) when the runtime
+// cannot say.  Every planning call (workspace query, plan query, the call
+// itself) asks, so on one device they all plan alike.
 int device_cus() {
   int dev = 0, n = 0;
   if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
@@ -142,9 +144,9 @@ int device_cus() {
 // lookup, page numbers, first copies, epilogue: several microseconds) besides
 // its keys, and splitting a request adds partial outputs and the combine
 // kernel; items are dispatched costliest request first, and one work group
-// fills a CU, so items run in rounds of 256.  The rule: the shortest chunk (a
-// multiple of the LDS buffer, at least 256 keys, at most S = all keys / 256,
-// one CU's share) whose items fit in two rounds -- the finest split that
+// fills a CU, so items run in rounds of `num_cus` (256 on MI355X).  The rule:
+// the shortest chunk (a multiple of the LDS buffer, at least 256 keys, at most
+// S = all keys / num_cus, one CU's share) whose items fit in two rounds -- the finest split that
 // leaves no third round for a few items to run alone; when even chunks of S
 // give more than two rounds, chunks of S (requests no longer than S stay
 // whole).  `pair_keys` holds T of every (request, column group); each stands
@@ -157,11 +159,11 @@ int device_cus() {
 // 24576-key chunks, a full chunk plus a short remainder per request, took
 // 1633 us against 1340 us whole), and finer chunks cost more than a dispatch
 // model with a fixed start-up predicts (merge work, partial traffic).
-int choose_chunk(const std::vector<int64_t>& pair_keys, int hkv) {
+int choose_chunk(const std::vector<int64_t>& pair_keys, int hkv, int num_cus) {
   const int forced = env_int("RG_ATTN_CHUNK", 0);
   if (forced > 0) return (int)std::min<int64_t>(kMaxChunkKeys, round_up(forced, kKeyTile));
-  constexpr int64_t kCUs = 256;
-  constexpr int64_t kTwoRounds = 2 * kCUs;
+  const int64_t kCUs = std::max(1, num_cus);
+  const int64_t kTwoRounds = 2 * kCUs;
   const int64_t floor_keys = round_up(std::max(kKeyTile, env_int("RG_ATTN_MIN_CHUNK", 256)), kKeyTile);
   int64_t total = 0, longest = 0;
   for (int64_t t : pair_keys) {
@@ -214,7 +216,7 @@ rg_status plan_attention(const rg_attn_layout* L, const rg_branch_layout* B, Ful
     const int64_t ncg = (n * g + fp.cols_per_group - 1) / fp.cols_per_group;
     for (int64_t cg = 0; cg < ncg; ++cg) pair_keys.push_back((int64_t)L->ctx_len[r] + n);
   }
-  fp.chunk = choose_chunk(pair_keys, hkv);
+  fp.chunk = choose_chunk(pair_keys, hkv, num_cus);
   // Costliest work items first: work groups are dispatched in item order, so
   // the long items start early and the short ones fill in at the end.  An
   // item's time is estimated in units of one 128-key buffer at the copy rate:
@@ -340,11 +342,11 @@ namespace {
 using FullPlan = FullPlanT<AttnPlan>;
 using FullPlanBr = FullPlanT<AttnPlanBr>;
 
-rg_status plan_plain(const rg_attn_layout* layout, FullPlan& fp, int num_cus = 256) {
+rg_status plan_plain(const rg_attn_layout* layout, FullPlan& fp, int num_cus) {
   return plan_attention<AttnPlan, kMaxReqPerLaunch>(layout, nullptr, fp, num_cus);
 }
 rg_status plan_branched(const rg_attn_layout* layout, const rg_branch_layout* branches, FullPlanBr& fp,
-                        int num_cus = 256) {
+                        int num_cus) {
   rg_status st = validate_branches(layout, branches);
   if (st != RG_OK) return st;
   return plan_attention<AttnPlanBr, kMaxReqPerLaunchBr>(layout, branches, fp, num_cus);
@@ -393,7 +395,7 @@ rg_status rg_draft_verify_attention_workspace(const rg_attn_layout* layout, size
   rg_status st = validate_layout(layout);
   if (st != RG_OK) return st;
   FullPlan fp;
-  st = plan_plain(layout, fp);
+  st = plan_plain(layout, fp, device_cus());
   if (st != RG_OK) return st;
   *bytes = fp.ws_bytes;
   return RG_OK;
@@ -404,7 +406,7 @@ rg_status rg_draft_verify_attention_plan(const rg_attn_layout* layout, rg_attn_p
   rg_status st = validate_layout(layout);
   if (st != RG_OK) return st;
   FullPlan fp;
-  st = plan_plain(layout, fp);
+  st = plan_plain(layout, fp, device_cus());
   if (st != RG_OK) return st;
   info->num_launches = (int32_t)fp.launches.size();
   info->chunk_keys = fp.chunk;
@@ -436,7 +438,7 @@ rg_status rg_multibranch_attention_workspace(const rg_attn_layout* layout, const
   rg_status st = validate_layout(layout);
   if (st != RG_OK) return st;
   FullPlanBr fp;
-  st = plan_branched(layout, branches, fp);
+  st = plan_branched(layout, branches, fp, device_cus());
   if (st != RG_OK) return st;
   *bytes = fp.ws_bytes;
   return RG_OK;

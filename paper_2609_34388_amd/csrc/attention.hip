@@ -197,7 +197,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
 
   const int r = find_request(p, item, false);
   const auto rq = p.req[r];
-  const int n = rq.nv & 0xffff, nver = rq.nv >> 16, L = rq.ctx, T = L + n;
+  // both counts are 16-bit fields of one word: unpack unsigned (n_verify may reach 65535)
+  const int n = rq.nv & 0xffff, nver = (int)((uint32_t)rq.nv >> 16), L = rq.ctx, T = L + n;
   const int g = a.g;
   const int M = n * g;
   const int ncg = (M + COLS - 1) / COLS;

@@ -28,7 +28,7 @@ constexpr int kSyncWords = kSyncHeader + 2 * kMaxSyncComb;
 struct AttnReq {
   int32_t q_start;     // first query row (token) of the request
   int32_t ctx;         // cached context tokens L
-  int32_t nv;          // n (low 16 bits) | n_verify << 16
+  int32_t nv;          // n (low 16 bits) | n_verify << 16, both unsigned 16-bit fields
   int32_t page_start;  // offset of the request's pages in page_indices
   int32_t item_start;  // first main-kernel work item
   int32_t part_start;  // first partial column in the workspace (split requests)

@@ -497,7 +497,8 @@ def make_logit_inputs(layout: Layout, device="cpu", *, sigma: Optional[float] = 
     return dict(verify_logits=verify, draft_tokens=tokens.contiguous(), draft_logits=draft)
 
 
-def make_mask_probe(layout: Layout, device="cpu", *, score_gap: float = 45.0) -> Dict[str, torch.Tensor]:
+def make_mask_probe(layout: Layout, device="cpu", *, score_gap: float = 45.0,
+                    poison: Optional[float] = None) -> Dict[str, torch.Tensor]:
     """Attention inputs whose softmax weights are known in closed form.
 
     Every cached context key has a zero first component; every key of the
@@ -505,10 +506,12 @@ def make_mask_probe(layout: Layout, device="cpu", *, score_gap: float = 45.0) ->
     ``s * e_0``.  With ``sm_scale * s * c = score_gap`` the new-row keys a
     query may see outweigh the context keys by about exp(score_gap), and all
     of them score the same, so a query's output is the plain mean of the
-    values of the new-row keys it may see.  Values stay random.
+    values of the new-row keys it may see.  Values stay random; ``poison``
+    as in ``make_attention_inputs`` (slots no request may read keep it in
+    every component but the first key component).
     """
     s = layout.spec
-    base = make_attention_inputs(layout, device)
+    base = make_attention_inputs(layout, device, poison=poison)
     q, k, v = base["q"], base["k_cache"], base["v_cache"]
     D = s.head_dim
     scale = 1.0 / math.sqrt(D)
@@ -517,15 +520,27 @@ def make_mask_probe(layout: Layout, device="cpu", *, score_gap: float = 45.0) ->
     q.zero_()
     q[:, :, 0] = mag
     k[:, :, :, 0] = 0.0
-    for r in range(layout.num_requests):
-        L = int(layout.ctx_len[r])
-        T = int(layout.kv_len[r])
-        p0 = int(layout.page_indptr[r])
-        for j in range(L, T):
-            page = int(layout.page_indices[p0 + j // PAGE_SIZE])
-            k[page, :, j % PAGE_SIZE, :] = 0.0
-            k[page, :, j % PAGE_SIZE, 0] = mag
+    pages, slots = new_row_slots(layout)
+    if len(pages):
+        pt = torch.as_tensor(pages, device=k.device)
+        st = torch.as_tensor(slots, device=k.device)
+        k[pt, :, st, :] = 0.0
+        k[pt, :, st, 0] = mag
     return dict(q=q, k_cache=k, v_cache=v, probe_magnitude=torch.tensor(mag))
+
+
+def new_row_slots(layout: Layout) -> Tuple[np.ndarray, np.ndarray]:
+    """(page, slot) of every new-row key (positions L .. T-1 of each
+    request), requests in order, positions ascending."""
+    pages, slots = [], []
+    for r in range(layout.num_requests):
+        L, T = int(layout.ctx_len[r]), int(layout.kv_len[r])
+        j = np.arange(L, T)
+        pages.append(layout.page_indices[int(layout.page_indptr[r]) + j // PAGE_SIZE].astype(np.int64))
+        slots.append(j % PAGE_SIZE)
+    if not pages:
+        return np.zeros(0, np.int64), np.zeros(0, np.int64)
+    return np.concatenate(pages), np.concatenate(slots).astype(np.int64)
 
 
 def bf16_bits(t: torch.Tensor) -> np.ndarray:

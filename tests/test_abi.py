@@ -87,6 +87,24 @@ def test_attention_validation_errors():
     assert _attn(_L(), q=ctypes.c_void_p(0x1002)) == 3
 
 
+@pytest.mark.parametrize("nv", [32767, 32768, 40000, 65535])
+def test_verify_counts_up_to_16_bits_are_planned(nv):
+    """A request's row count and verify count share one packed plan word
+    (16 bits each); every verify count up to 65535 is accepted and planned
+    like any other layout (the kernel reads the field unsigned)."""
+    l = _L(R=1, hq=1, hkv=1, D=64, ctx=(16,), nv=(nv,), n=(nv,), num_pages=(16 + nv) // 16 + 2)
+    info = _plan(l)
+    assert info.work_items >= 1
+    assert _attn(l, out=None) == 1  # validation passes up to the pointer checks
+
+
+def test_row_counts_past_16_bits_are_rejected():
+    l = _L(R=1, hq=1, hkv=1, D=64, ctx=(0,), nv=(0,), n=(65536,), num_pages=4097)
+    st = binding.library().rg_draft_verify_attention_workspace(ctypes.byref(l.c), ctypes.byref(ctypes.c_size_t()))
+    assert st == 3
+    assert _attn(l) == 3
+
+
 def _br(indptr, prefix, lead, rows):
     return binding.make_branches(indptr, prefix, lead, rows)
 
@@ -247,9 +265,11 @@ def test_plan_chunk_override_and_workspace_monotone(monkeypatch):
 @pytest.mark.parametrize("persist", ["1", "0"])
 @pytest.mark.parametrize("name", ["low", "mid", "high"])
 def test_plan_one_launch_mode_and_sync_words(monkeypatch, persist, name):
-    """Launches with a split request run as one work-queue launch unless
-    RG_ATTN_PERSIST=0; the synchronisation words (queue head, exit count,
-    error word, then two counters per merge item) sit after the partials."""
+    """Launches with a split request run as one work-queue launch when
+    RG_ATTN_PERSIST=1 (the default is the main kernel plus the merge
+    kernel); the synchronisation words (queue head, exit count, error word,
+    then two counters per merge item) open the workspace at a fixed place
+    and size, before the partials."""
     monkeypatch.setenv("RG_ATTN_PERSIST", persist)
     lay = W.make_layout(name, seed=1)
     s = lay.spec

@@ -139,6 +139,94 @@ def test_mask_probe(kind):
     check(out, lse, reference(lay, inp))
 
 
+def probe_closed_form(lay, inp, r):
+    """What the mask probe fixes for request r, from the definition alone:
+    every visible new-row key scores the same and the context is e^-45 or
+    less behind, so verify row i returns the mean of the values at keys
+    L .. L + i, a draft row the mean over L .. T - 1, and the log-sum-exp is
+    the new-row score plus the log of the number of keys averaged.  Returns
+    (out [n, Hq, D], lse [n, Hq]) in float64 on the device."""
+    s = lay.spec
+    g = s.num_q_heads // s.num_kv_heads
+    L, V, n = int(lay.ctx_len[r]), int(lay.n_verify[r]), int(lay.q_len[r])
+    j = np.arange(L, L + n)
+    pages = torch.as_tensor(lay.page_indices[int(lay.page_indptr[r]) + j // 16].astype(np.int64), device=DEV)
+    slots = torch.as_tensor(j % 16, device=DEV)
+    vals = inp["v_cache"][pages, :, :, slots].double()          # [n, Hkv, D]
+    cnt = torch.arange(1, n + 1, device=DEV, dtype=torch.float64)
+    means = vals.cumsum(0) / cnt[:, None, None]                  # mean over the first i + 1 new keys
+    seen = torch.as_tensor(np.where(np.arange(n) < V, np.arange(n), n - 1), device=DEV)
+    out = means[seen].repeat_interleave(g, dim=1)                # query head h reads KV head h // g
+    mag = float(inp["probe_magnitude"])
+    scale = 1.0 / np.sqrt(s.head_dim)
+    lse = (scale * mag * mag + torch.log(cnt[seen].double()))[:, None].expand(n, s.num_q_heads)
+    return out, lse
+
+
+def check_probe(out, lse, want_out, want_lse):
+    got = out.double()
+    norm = want_out.norm(dim=-1).clamp_min(1e-6)
+    err = (got - want_out).abs().amax(-1) / norm
+    assert torch.isfinite(got).all()
+    assert err.max().item() <= ATOL_ROW, f"probe row error {err.max().item():.3e}"
+    assert (lse.double() - want_lse).abs().max().item() <= LSE_ATOL
+    return err.max().item()
+
+
+@pytest.mark.parametrize("ctx", [4096, 4088])
+def test_mask_probe_full_low_shape(ctx):
+    """The batch-1 benchmark shape (32 / 8 heads, D = 128, 16 verify + 16
+    draft rows) under the closed-form probe, launched as the benchmark
+    launches it (256-key chunks, 17 of them): the closed form on every row
+    and head, and the oracle on the whole request.  With 4088 context tokens
+    the 4096-key chunk boundary falls between verify rows 7 and 8, so the
+    mask is checked on both sides of a split."""
+    lay = W.make_layout("low", seed=6, ctx=("fixed", ctx))
+    inp = W.make_mask_probe(lay, DEV, poison=float("nan"))
+    info = binding.attention_plan(binding.make_layout(inp["q"], inp["k_cache"], lay.q_indptr, lay.n_verify,
+                                                      lay.ctx_len, lay.page_indptr,
+                                                      torch.as_tensor(lay.page_indices, device=DEV)))
+    assert info["split_requests"] == 1 and info["chunk_keys"] == 256
+    out, lse = run(lay, inp)
+    check_probe(out, lse, *probe_closed_form(lay, inp, 0))
+    check(out, lse, reference(lay, inp))
+
+
+def test_mask_probe_full_long_shape():
+    """The largest benchmark shape (64 requests, 16k-32k context tokens)
+    under the closed-form probe: every row and head of every request against
+    the closed form, and two sampled requests against the oracle.  Here a
+    one-key leak would move an output by far less than the 1e-2 tolerance on
+    random inputs; under the probe it changes a weight from 1/(i+1) to
+    1/(i+2)."""
+    lay = W.make_layout("long", seed=0)
+    inp = W.make_mask_probe(lay, DEV, poison=float("nan"))
+    out, lse = run(lay, inp)
+    for r in range(lay.num_requests):
+        q0, q1 = int(lay.q_indptr[r]), int(lay.q_indptr[r + 1])
+        check_probe(out[q0:q1], lse[q0:q1], *probe_closed_form(lay, inp, r))
+    for r in (int(np.argmax(lay.kv_len)), int(np.argmax(lay.q_len))):
+        sub, qi, pi, pidx = _sub_problem(lay, inp, r)
+        ref = oracle.oracle_attention(W.bf16_bits(sub["q"]), W.bf16_bits(sub["k_cache"]),
+                                      W.bf16_bits(sub["v_cache"]), qi, lay.n_verify[r:r + 1],
+                                      lay.ctx_len[r:r + 1], pi, pidx)
+        q0, q1 = int(lay.q_indptr[r]), int(lay.q_indptr[r + 1])
+        check(out[q0:q1], lse[q0:q1], ref)
+
+
+def test_verify_rows_past_32767():
+    """40000 verify rows (and 8 draft rows) in one request: the verify count
+    fills the upper 16 bits of the packed per-request word, which must be
+    read unsigned (as a signed field it would turn negative and give every
+    verify row the draft rows' bidirectional mask).  Checked on every row
+    against the probe's closed form (the dense oracle would need a
+    40008 x 40024 mask)."""
+    lay = _custom(1, [16], [40000], [8], hq=1, hkv=1, D=64)
+    inp = W.make_mask_probe(lay, DEV, poison=float("nan"))
+    out, lse = run(lay, inp)
+    check_probe(out, lse, *probe_closed_form(lay, inp, 0))
+
+
 def test_sharp_scores():
     lay = W.make_layout("mid", seed=7, num_requests=3, ctx=("uniform", 100, 400))
     inp = W.make_attention_inputs(lay, DEV, poison=float("nan"), qk_std=1.0)

@@ -212,13 +212,15 @@ def test_plan_and_match_branches_match_oracle(seed):
     assert (want_r >= 0).sum() > R // 10  # the outcomes above do hit branches
 
 
-@pytest.mark.parametrize("workload", ["mid", "high"])
+@pytest.mark.parametrize("workload", ["mid", "high", "long"])
 def test_overlap_round_full_size(workload):
     """A full-size overlap round (every request with two correction branches
     and a continuation, the layout the benchmark times): sampled requests
     against the oracle, and every row against the same rows served as
     separate requests (each branch with its own copy of the kept prefix)
-    through rg_draft_verify_attention."""
+    through rg_draft_verify_attention.  At `long` the sampled requests
+    include the one with the most rows (several 256-column groups) and the
+    one with the most keys."""
     lay = W.make_layout(workload, seed=4)
     branches = W.overlap_branches(lay)
     ov = W.make_overlap_layout(lay, branches)
@@ -226,6 +228,9 @@ def test_overlap_round_full_size(workload):
     out, lse = _run(ov, inp, branches)
     rng = np.random.default_rng(4)
     reqs = sorted(rng.choice(ov.num_requests, size=min(3, ov.num_requests), replace=False).tolist())
+    if workload == "long":
+        reqs = sorted(set(reqs) | {int(np.argmax(ov.q_len)), int(np.argmax(ov.kv_len))})
+        assert int(ov.q_len.max()) * (ov.spec.num_q_heads // ov.spec.num_kv_heads) > 256
     heads = [0, 13, 31]
     ref = oracle.oracle_branch_attention(W.bf16_bits(inp["q"]), W.bf16_bits(inp["k_cache"]),
                                          W.bf16_bits(inp["v_cache"]), ov.q_indptr, ov.n_verify, ov.ctx_len,
