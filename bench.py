@@ -6,13 +6,16 @@ A step is the whole hot path over one batch: hybrid-mask paged attention
 confidence, both logit passes of the round in one call
 (rg_verify_and_confidence: the same results as rg_verify_accept followed by
 rg_draft_confidence, in two launches instead of four).  The separate calls
-are timed too.  Inputs are
-seeded synthetic tensors resident in HBM before timing starts; several
-copies of every input are rotated through the steps so that the working
-set exceeds the 256 MB Infinity Cache and the numbers are HBM numbers.
-Where one copy of the inputs fits in that cache, ``warm_cache`` reports the
-step, the attention call and the logit round with one copy reused by every
-call, labelled as such (context only).
+are timed too.  Inputs are seeded synthetic tensors resident in HBM before
+timing starts; several copies of every input are rotated through the steps
+so that the working set exceeds the 256 MB Infinity Cache and the numbers
+are HBM numbers.  Where one copy of the inputs fits in that cache,
+``warm_cache`` reports the step, the attention call and the logit round with
+one copy reused by every call, labelled as such (context only).
+
+The default workload is ``long`` (64 requests, 16k-32k context tokens, the
+largest configuration); ``all_configs`` reports every configuration's step,
+attention and logit-round figures from the same run.
 
 Prints one JSON line.  ``value`` is the step's achieved fraction of the HBM
 roofline (algorithmic bytes of all three calls / step time / 8 TB/s), in
@@ -20,12 +23,16 @@ percent; the attention call's TFLOP/s and GB/s and the logit passes' GB/s
 are reported beside it.  The timed region replays a HIP graph of exactly
 ``--steps`` steps between two HIP events on the capturing stream; each entry
 point is then timed the same way from a graph of ``--steps`` calls of it
-alone.  ``roofline`` covers the attention call (the dominant one): its
-algorithmic bytes over its per-call time.  ``roofline.traffic`` is the HBM
-traffic per call measured with rocprofv3 counters (FETCH_SIZE + WRITE_SIZE,
-scaled by what the same counters read for a plain copy of known size); it
-is read from the committed profile summary and reported only while the
-attention sources still hash to the ones that summary was taken with.
+alone.  Beside these means, ``*_event_median`` is the median over
+``--steps`` eager calls, each between its own pair of HIP events.
+``attention_host`` is the host time of the attention entry point (planning
+alone, and call to return).  ``roofline`` covers the attention call (the
+dominant one): its algorithmic bytes over its per-call time.
+``roofline.traffic`` is the HBM traffic per call measured with rocprofv3
+counters (FETCH_SIZE + WRITE_SIZE, scaled by what the same counters read for
+a plain copy of known size); it is read from the committed profile
+summaries and reported only while the attention sources still hash to the
+ones the counters were taken with.
 
 The ``overlap`` object measures the predictive draft-verify overlap on the
 same workload (rg_multibranch_attention over every request's verify rows and
@@ -59,7 +66,7 @@ CACHE_DEFEAT_BYTES = 512 << 20
 WARM_FIT_BYTES = 128 << 20  # one input copy this small stays in the 256 MB Infinity Cache
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_low_traffic.md")
+PROFILES = os.path.join(ROOT, "profiles")
 ATTN_SOURCES = ("attention.hip", "rg_internal.h", "api.cpp")
 
 
@@ -74,16 +81,25 @@ def attention_source_hash():
     return h.hexdigest()
 
 
+def traffic_records():
+    """Every TRAFFIC_JSON record of the committed counter summaries."""
+    import glob
+
+    recs = []
+    for path in sorted(glob.glob(os.path.join(PROFILES, "*.md"))):
+        for line in open(path):
+            if line.startswith("TRAFFIC_JSON "):
+                recs.append(json.loads(line[len("TRAFFIC_JSON "):]))
+    return recs
+
+
 def measured_traffic(workload):
-    """HBM bytes per attention call from the committed counter summary, or
+    """HBM bytes per attention call from the committed counter summaries, or
     None when there is none for this workload or the sources changed since."""
-    if not os.path.exists(TRAFFIC_FILE):
-        return None
-    for line in open(TRAFFIC_FILE):
-        if line.startswith("TRAFFIC_JSON "):
-            rec = json.loads(line[len("TRAFFIC_JSON "):])
-            if rec.get("workload") == workload and rec.get("source_sha256") == attention_source_hash():
-                return rec["hbm_bytes_per_call"]
+    h = attention_source_hash()
+    for rec in traffic_records():
+        if rec.get("workload") == workload and rec.get("source_sha256") == h:
+            return rec["hbm_bytes_per_call"]
     return None
 
 
@@ -355,66 +371,111 @@ def block_sizing_leg(lay, dev, timed):
                           "padded_to_largest": round(padded_us, 3)},
     }
 
+def _request_problem(lay, inputs, r):
+    """Request r of the batch as a problem of its own, as host bf16 bits: its
+    query rows, its pages of the K/V pools (renumbered 0 .. p-1), its verify
+    rows with the tokens they judge, and its next-block draft rows.  Input
+    preparation only (a gather and a copy), outside any timed region."""
+    import numpy as np
+    import torch
+
+    from paper_2609_34388_amd import workloads as W
+
+    p0, p1 = int(lay.page_indptr[r]), int(lay.page_indptr[r + 1])
+    q0, q1 = int(lay.q_indptr[r]), int(lay.q_indptr[r + 1])
+    v0, v1 = int(lay.row_indptr[r]), int(lay.row_indptr[r + 1])
+    d0, d1 = int(lay.draft_row_indptr[r]), int(lay.draft_row_indptr[r + 1])
+    pages = torch.as_tensor(lay.page_indices[p0:p1].astype(np.int64), device=inputs["k_cache"].device)
+    return dict(q=W.bf16_bits(inputs["q"][q0:q1]), k=W.bf16_bits(inputs["k_cache"][pages]),
+                v=W.bf16_bits(inputs["v_cache"][pages]), q_indptr=np.array([0, q1 - q0], np.int32),
+                page_indptr=np.array([0, p1 - p0], np.int32), page_indices=np.arange(p1 - p0, dtype=np.int32),
+                n_verify=lay.n_verify[r:r + 1], ctx_len=lay.ctx_len[r:r + 1],
+                verify=W.bf16_bits(inputs["verify_logits"][v0:v1]), row_indptr=np.array([0, v1 - v0], np.int32),
+                tokens=inputs["draft_tokens"][v0:v1].cpu().numpy(), draft=W.bf16_bits(inputs["draft_logits"][d0:d1]))
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        return 1
+
+
 def cpu_baseline(lay, inputs, budget_s: float):
-    """The fp64 oracle as it stands, timed on this host for whole steps of
-    the same workload (bounded by ``budget_s`` of CPU time)."""
+    """The fp64 oracle as it stands, timed on this host over the step's
+    three parts request by request (attention, acceptance, confidence of
+    request r's rows), requests in a seeded random order, until about
+    ``budget_s`` seconds of oracle time are spent (each request at most once
+    per pass; a batch of one request is run several times).  Requests are
+    independent draws of the workload, so the whole step's oracle time is
+    estimated as the mean time per request times the number of requests."""
     import numpy as np
 
     import oracle
-    from paper_2609_34388_amd import workloads as W
 
-    try:
-        from threadpoolctl import threadpool_info
-        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        blas_threads = 1
-    q, k, v = (W.bf16_bits(inputs[n]) for n in ("q", "k_cache", "v_cache"))
-    vl, dl = W.bf16_bits(inputs["verify_logits"]), W.bf16_bits(inputs["draft_logits"])
-    tok = inputs["draft_tokens"].cpu().numpy()
-    runs, t_total = 0, 0.0
+    R = lay.num_requests
+    order = np.random.default_rng(12345).permutation(R)
     parts = [0.0, 0.0, 0.0]  # attention, accept, confidence
-    while runs == 0 or (t_total < budget_s and runs < 50):
+    done = 0
+    while done == 0 or (sum(parts) < budget_s and done < max(R, 50)):
+        r = int(order[done % R])
+        pb = _request_problem(lay, inputs, r)
         t0 = time.perf_counter()
-        oracle.oracle_attention(q, k, v, lay.q_indptr, lay.n_verify, lay.ctx_len, lay.page_indptr,
-                                lay.page_indices)
+        oracle.oracle_attention(pb["q"], pb["k"], pb["v"], pb["q_indptr"], pb["n_verify"], pb["ctx_len"],
+                                pb["page_indptr"], pb["page_indices"])
         t1 = time.perf_counter()
-        oracle.oracle_accept(vl, lay.row_indptr, tok)
+        oracle.oracle_accept(pb["verify"], pb["row_indptr"], pb["tokens"])
         t2 = time.perf_counter()
-        oracle.oracle_confidence(dl)
+        oracle.oracle_confidence(pb["draft"])
         t3 = time.perf_counter()
         for j, dt in enumerate((t1 - t0, t2 - t1, t3 - t2)):
             parts[j] += dt
-        t_total += t3 - t0
-        runs += 1
-    split = {"oracle_attention_ms": round(parts[0] / runs * 1e3, 2),
-             "oracle_accept_ms": round(parts[1] / runs * 1e3, 2),
-             "oracle_confidence_ms": round(parts[2] / runs * 1e3, 2)}
-    return t_total / runs, runs, blas_threads, len(os.sched_getaffinity(0)), split
+        done += 1
+    per_req = [p / done for p in parts]
+    distinct = min(done, R)
+    return {"step_s": sum(per_req) * R, "requests_timed": done, "distinct_requests": distinct,
+            "oracle_attention_ms": round(per_req[0] * R * 1e3, 2),
+            "oracle_accept_ms": round(per_req[1] * R * 1e3, 2),
+            "oracle_confidence_ms": round(per_req[2] * R * 1e3, 2),
+            "blas_threads": blas_threads(), "visible_cores": len(os.sched_getaffinity(0)),
+            "sample": (f"{done} request run(s) ({distinct} distinct of {R}; all heads and rows of each) of the "
+                       f"fp64 numpy oracle, {sum(parts):.1f} s in all; whole-step time = mean time per request "
+                       f"x {R} requests")}
 
 
-def cpu_baseline_rows(lay, budget_s: float):
+def cpu_baseline_rows(lay, dev, budget_s: float):
     """The oracle beside the rows built past the step, on the same workload:
     the overlap round's multi-branch attention (request by request, within
-    ``budget_s``; inputs of the same shapes drawn on the host) and one
-    block-sizing round for every request."""
+    ``budget_s``; inputs drawn on the device, each timed request's keys and
+    rows copied to the host first) and one block-sizing round for every
+    request."""
     import numpy as np
+    import torch
 
     import oracle
     from paper_2609_34388_amd import workloads as W
 
     branches = W.overlap_branches(lay)
     ov = W.make_overlap_layout(lay, branches)
-    host = W.make_attention_inputs(ov, "cpu")
-    q, k, v = (W.bf16_bits(host[n]) for n in ("q", "k_cache", "v_cache"))
+    inp = W.make_attention_inputs(ov, dev)
     done, t_total = 0, 0.0
-    for r in range(ov.num_requests):
+    order = np.random.default_rng(12345).permutation(ov.num_requests)
+    for r in order:
+        r = int(r)
+        p0, p1 = int(ov.page_indptr[r]), int(ov.page_indptr[r + 1])
+        q0, q1 = int(ov.q_indptr[r]), int(ov.q_indptr[r + 1])
+        pages = torch.as_tensor(ov.page_indices[p0:p1].astype(np.int64), device=inp["k_cache"].device)
+        qb, kb, vb = (W.bf16_bits(t) for t in (inp["q"][q0:q1], inp["k_cache"][pages], inp["v_cache"][pages]))
         t0 = time.perf_counter()
-        oracle.oracle_branch_attention(q, k, v, ov.q_indptr, ov.n_verify, ov.ctx_len, ov.page_indptr,
-                                       ov.page_indices, branches, requests=[r])
+        oracle.oracle_branch_attention(qb, kb, vb, np.array([0, q1 - q0], np.int32), ov.n_verify[r:r + 1],
+                                       ov.ctx_len[r:r + 1], np.array([0, p1 - p0], np.int32),
+                                       np.arange(p1 - p0, dtype=np.int32), [branches[r]])
         t_total += time.perf_counter() - t0
         done += 1
         if t_total >= budget_s:
             break
+    del inp
     overlap = {"us_per_request": round(t_total / done * 1e6, 1), "requests_timed": done,
                "us_all_requests_estimated": round(t_total / done * ov.num_requests * 1e6, 1),
                "sample": f"{done} of {ov.num_requests} request(s) of the overlap round (verify rows and three "
@@ -429,48 +490,56 @@ def cpu_baseline_rows(lay, budget_s: float):
     return {"overlap_multibranch_attention": overlap, "plan_block_sizes": sizing}
 
 
-def main(argv=None):
-    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="low",
-                    help="tiny | low | low_sigma2 | mid | high | long (default: low, C = 1, B = 16)")
-    ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--copies", type=int, default=0, help="input copies rotated (0 = enough for 512 MB)")
-    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-overlap", action="store_true", help="skip the overlap-round measurement")
-    ap.add_argument("--no-block-sizing", action="store_true", help="skip the block-sizing measurement")
-    ap.add_argument("--copy-calibration-mb", type=int, default=0,
-                    help="run a plain copy of this many MiB (counter calibration) and exit")
-    args = ap.parse_args(argv)
+def host_call_times(layout, q, k, v, out, lse, ws, stream, n):
+    """Host cost of the attention entry point (row a1, the planning): the
+    mean time of rg_draft_verify_attention_plan (validation and planning, no
+    GPU work), and of rg_draft_verify_attention itself from call to return
+    (validation, planning and the kernel launches; the kernels run
+    asynchronously), over n calls each, called through ctypes directly."""
+    import ctypes
 
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: the library has no multi-GPU path "
-              "(requests and KV heads would shard across GPUs with no exchange).", file=sys.stderr)
-        return 2
+    import torch
 
-    if args.copy_calibration_mb > 0:
-        return copy_calibration(args.copy_calibration_mb)
+    from paper_2609_34388_amd import binding
 
+    lib = binding.library()
+    info = binding.AttnPlanInfo()
+    ref = ctypes.byref(layout.c)
+    t0 = time.perf_counter()
+    for _ in range(n):
+        lib.rg_draft_verify_attention_plan(ref, ctypes.byref(info))
+    plan_us = (time.perf_counter() - t0) / n * 1e6
+    ws_ptr = ws.data_ptr() if ws is not None else None
+    ws_bytes = ws.numel() if ws is not None else 0
+    args = (ref, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(), ws_ptr, ws_bytes,
+            stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(n):
+        st = lib.rg_draft_verify_attention(*args)
+    call_us = (time.perf_counter() - t0) / n * 1e6
+    torch.cuda.synchronize()
+    if st != 0:
+        raise RuntimeError(f"rg_draft_verify_attention returned {st}")
+    return {"plan_us": round(plan_us, 2), "call_us": round(call_us, 2), "calls": n,
+            "note": "host time per call (rg_draft_verify_attention_plan alone; the attention call from "
+                    "call to return, its kernels running asynchronously)"}
+
+
+def measure_workload(name, seed, dev, steps, warmup, copies_arg=0, detail=False):
+    """Time one workload's step and its entry points.  Returns the results
+    and, with ``detail``, the objects the extra legs reuse."""
     import torch
 
     from paper_2609_34388_amd import binding
     from paper_2609_34388_amd import workloads as W
 
-    if not os.path.exists(binding.LIB_PATH):
-        from paper_2609_34388_amd import build_lib
-        build_lib.build()
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-
-    lay = W.make_layout(args.workload, seed=args.seed)
+    lay = W.make_layout(name, seed=seed)
     s = lay.spec
     base = W.make_attention_inputs(lay, dev)
     base.update(W.make_logit_inputs(lay, dev))
     per_copy = sum(t.numel() * t.element_size() for t in base.values())
-    copies = args.copies or max(1, math.ceil(CACHE_DEFEAT_BYTES / per_copy))
+    copies = copies_arg or max(1, math.ceil(CACHE_DEFEAT_BYTES / per_copy))
     sets = [base] + [{k: t.clone() for k, t in base.items()} for _ in range(copies - 1)]
     page_idx = torch.as_tensor(lay.page_indices, device=dev)
     row_indptr = torch.as_tensor(lay.row_indptr, device=dev)
@@ -517,55 +586,162 @@ def main(argv=None):
         logit_round(i)
 
     # Warmup: eager steps (compiles nothing; loads the library, touches every buffer).
-    for i in range(args.warmup):
+    for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
 
     # The step is launch-bound at low concurrency, so the timed region replays a
-    # HIP graph holding exactly `steps` captured steps (input copies rotated).
-    def capture(fn, n, base):
+    # HIP graph holding exactly `steps` captured steps (input copies rotated),
+    # between two HIP events on the capturing stream.
+    def capture(fn, n, first):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             for i in range(n):
-                fn(base + i)
+                fn(first + i)
         torch.cuda.synchronize()
         return g
 
-    g_step = capture(step, args.steps, args.warmup)
-    stream = torch.cuda.current_stream()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    g_step.replay()
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    ms_step = t_start.elapsed_time(t_end) / args.steps
-
-    # Per-call times: graphs of `steps` calls of one entry point each, timed
-    # with HIP events on the same stream right after the step graph.
     def time_calls(fn):
-        g = capture(fn, args.steps, args.warmup)
+        g = capture(fn, steps, warmup)
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
         e0.record(stream)
         g.replay()
         e1.record(stream)
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / args.steps
+        del g
+        return e0.elapsed_time(e1) / steps
 
+    def event_median(fn):
+        """Median over `steps` eager calls, each between its own pair of HIP
+        events on the launching stream (launch gaps between calls excluded,
+        each call's own launches included)."""
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(ev):
+            a.record(stream)
+            fn(warmup + i)
+            b.record(stream)
+        torch.cuda.synchronize()
+        t = sorted(a.elapsed_time(b) for a, b in ev)
+        return t[len(t) // 2] if len(t) % 2 else 0.5 * (t[len(t) // 2 - 1] + t[len(t) // 2])
+
+    ms_step = time_calls(step)
     attn_ms = time_calls(attention)
-    ver_ms = time_calls(verify)
-    dr_ms = time_calls(draft)
     round_ms = time_calls(logit_round)
+    step_med = event_median(step)
+    attn_med = event_median(attention)
 
     work = algorithmic_work(lay)
     step_bytes = work["attn_bytes"] + work["verify_bytes"] + work["draft_bytes"]
+    logit_bytes = work["verify_bytes"] + work["draft_bytes"]
+    gbps = lambda b, ms: b / (ms * 1e-3) / 1e9
+    plan = binding.attention_plan(layouts[0])
+    res = dict(
+        lay=lay, work=work, step_bytes=step_bytes, copies=copies, per_copy=per_copy, plan=plan,
+        ms_step=ms_step, attn_ms=attn_ms, round_ms=round_ms, step_med=step_med, attn_med=attn_med,
+        summary={"step_us": round(ms_step * 1e3, 3), "step_us_event_median": round(step_med * 1e3, 3),
+                 "value": round(100.0 * gbps(step_bytes, ms_step) / HBM_PEAK_GBPS, 3),
+                 "attention_us": round(attn_ms * 1e3, 3), "attention_us_event_median": round(attn_med * 1e3, 3),
+                 "attention_frac_hbm": round(gbps(work["attn_bytes"], attn_ms) / HBM_PEAK_GBPS, 4),
+                 "attention_tflops": round(work["attn_flops"] / (attn_ms * 1e-3) / 1e12, 3),
+                 "logit_round_us": round(round_ms * 1e3, 3),
+                 "logits_frac_hbm": round(gbps(logit_bytes, round_ms) / HBM_PEAK_GBPS, 4),
+                 "requests": lay.num_requests, "input_copies_rotated": copies})
+    if not detail:
+        del sets, layouts
+        return res
+    res["ver_ms"] = time_calls(verify)
+    res["dr_ms"] = time_calls(draft)
+    res["host"] = host_call_times(layouts[0], sets[0]["q"], sets[0]["k_cache"], sets[0]["v_cache"], out, lse,
+                                  attn_ws, stream.cuda_stream, n=100 if lay.num_requests > 16 else 400)
+    if plan["split_requests"] > 0:
+        # The one-launch work-queue mode (split chunks merged in the same
+        # launch), opt-in through RG_ATTN_PERSIST=1, timed the same way.
+        prev = os.environ.get("RG_ATTN_PERSIST")
+        os.environ["RG_ATTN_PERSIST"] = "1"
+        try:
+            one_ms = time_calls(attention)
+            one_plan = binding.attention_plan(layouts[0])
+        finally:
+            if prev is None:
+                del os.environ["RG_ATTN_PERSIST"]
+            else:
+                os.environ["RG_ATTN_PERSIST"] = prev
+        res["attention_one_launch"] = {"us": round(one_ms * 1e3, 3),
+                                       "persistent_launches": one_plan["persistent_launches"],
+                                       "time_vs_two_launches": round(one_ms / attn_ms, 3)}
+    if copies > 1 and per_copy <= WARM_FIT_BYTES:
+        # Labelled warm-cache figures, never the headline: every call of the
+        # graph reuses input copy 0, which then stays in the Infinity Cache.
+        warm_step = time_calls(lambda i: step(0))
+        warm_attn = time_calls(lambda i: attention(0))
+        warm_round = time_calls(lambda i: logit_round(0))
+        res["warm_cache"] = {
+            "note": "inputs resident in the 256 MB Infinity Cache (one input copy reused by every call); "
+                    "context only, the headline numbers above rotate copies past the cache",
+            "input_bytes": per_copy, "ms_per_step": round(warm_step, 5),
+            "attention_us": round(warm_attn * 1e3, 3),
+            "attention_gbps": round(work["attn_bytes"] / (warm_attn * 1e-3) / 1e9, 1),
+            "logit_round_us": round(warm_round * 1e3, 3)}
+    res.update(capture=capture, time_calls=time_calls, vout=vout, dout=dout,
+               host_inputs={k: base[k] for k in ("q", "k_cache", "v_cache", "verify_logits", "draft_logits",
+                                                 "draft_tokens")})
+    return res
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="long",
+                    help="tiny | low | low_sigma2 | mid | high | long (default: long, the largest configuration: "
+                         "64 requests, 16k-32k context tokens)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copies", type=int, default=0, help="input copies rotated (0 = enough for 512 MB)")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-overlap", action="store_true", help="skip the overlap-round measurement")
+    ap.add_argument("--no-block-sizing", action="store_true", help="skip the block-sizing measurement")
+    ap.add_argument("--no-all-configs", action="store_true",
+                    help="skip the per-workload summary of the other configurations")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="run a plain copy of this many MiB (counter calibration) and exit")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
+              "(requests and KV heads would shard across GPUs with no exchange).", file=sys.stderr)
+        return 2
+
+    if args.copy_calibration_mb > 0:
+        return copy_calibration(args.copy_calibration_mb)
+
+    import torch
+
+    from paper_2609_34388_amd import binding
+
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2609_34388_amd import build_lib
+        build_lib.build()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_start = time.perf_counter()
+
+    m = measure_workload(args.workload, args.seed, dev, args.steps, args.warmup, args.copies, detail=True)
+    lay, work, plan = m["lay"], m["work"], m["plan"]
+    s = lay.spec
+    ms_step, attn_ms, round_ms = m["ms_step"], m["attn_ms"], m["round_ms"]
+    ver_ms, dr_ms = m["ver_ms"], m["dr_ms"]
+    step_bytes = m["step_bytes"]
     step_gbps = step_bytes / (ms_step * 1e-3) / 1e9
     attn_gbps = work["attn_bytes"] / (attn_ms * 1e-3) / 1e9
     attn_tflops = work["attn_flops"] / (attn_ms * 1e-3) / 1e12
-    plan = binding.attention_plan(layouts[0])
     traffic = measured_traffic(args.workload) if args.seed == 0 else None
+    kernels = "attn_fwd_kernel + attn_combine_kernel" if plan["split_requests"] else "attn_fwd_kernel"
 
     result = {
         "metric": "draft-verify attention TFLOP/s + logits GB/s, % of MI355X roofline, 1 GPU",
@@ -580,17 +756,22 @@ def main(argv=None):
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "timing": "HIP graph replay of the timed steps (and of each entry point alone for per-call times)",
+        "timing": "mean over a HIP graph replay of exactly `steps` captured steps between two HIP events "
+                  "(each entry point timed the same way alone); *_event_median: median over `steps` eager "
+                  "calls, each between its own HIP event pair",
         "config": {"workload": args.workload, "requests": lay.num_requests, "q_heads": s.num_q_heads,
                    "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "page_size": 16,
                    "context_tokens": int(lay.ctx_len.sum()), "verify_rows": int(lay.n_verify.sum()),
                    "draft_rows": int(lay.n_draft.sum()), "vocab": s.vocab, "seed": args.seed,
-                   "input_copies_rotated": copies, "attn_chunk_keys": plan["chunk_keys"],
+                   "input_copies_rotated": m["copies"], "attn_chunk_keys": plan["chunk_keys"],
                    "attn_work_items": plan["work_items"]},
-        "attention": {"ms": round(attn_ms, 5), "tflops": round(attn_tflops, 3), "gbps": round(attn_gbps, 1),
+        "step_ms_event_median": round(m["step_med"], 5),
+        "attention": {"ms": round(attn_ms, 5), "ms_event_median": round(m["attn_med"], 5),
+                      "tflops": round(attn_tflops, 3), "gbps": round(attn_gbps, 1),
                       "bytes": work["attn_bytes"], "flops": work["attn_flops"],
                       "frac_hbm": round(attn_gbps / HBM_PEAK_GBPS, 4),
                       "frac_mfma_bf16": round(attn_tflops / BF16_PEAK_TFLOPS, 5)},
+        "attention_host": m["host"],
         "verify_accept": {"ms": round(ver_ms, 5), "bytes": work["verify_bytes"],
                           "gbps": round(work["verify_bytes"] / (ver_ms * 1e-3) / 1e9, 1)},
         "draft_confidence": {"ms": round(dr_ms, 5), "bytes": work["draft_bytes"],
@@ -598,58 +779,54 @@ def main(argv=None):
         "logit_round": {"ms": round(round_ms, 5), "bytes": work["verify_bytes"] + work["draft_bytes"],
                         "gbps": round((work["verify_bytes"] + work["draft_bytes"]) / (round_ms * 1e-3) / 1e9, 1)},
         "logits_gbps": round((work["verify_bytes"] + work["draft_bytes"]) / (round_ms * 1e-3) / 1e9, 1),
-        "roofline": {"kernel": "rg_draft_verify_attention (attn_fwd_kernel + attn_combine_kernel)",
+        "roofline": {"kernel": f"rg_draft_verify_attention ({kernels})",
                      "bound": "hbm", "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(attn_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "algorithmic_bytes": work["attn_bytes"], "us_per_call": round(attn_ms * 1e3, 3)},
     }
-    if plan["split_requests"] > 0:
-        # The one-launch work-queue mode (split chunks merged in the same
-        # launch), opt-in through RG_ATTN_PERSIST=1, timed the same way.
-        prev = os.environ.get("RG_ATTN_PERSIST")
-        os.environ["RG_ATTN_PERSIST"] = "1"
-        try:
-            one_ms = time_calls(attention)
-            one_plan = binding.attention_plan(layouts[0])
-        finally:
-            if prev is None:
-                del os.environ["RG_ATTN_PERSIST"]
-            else:
-                os.environ["RG_ATTN_PERSIST"] = prev
-        result["attention_one_launch"] = {"us": round(one_ms * 1e3, 3),
-                                          "persistent_launches": one_plan["persistent_launches"],
-                                          "time_vs_two_launches": round(one_ms / attn_ms, 3)}
-    if copies > 1 and per_copy <= WARM_FIT_BYTES:
-        # Labelled warm-cache figures, never the headline: every call of the
-        # graph reuses input copy 0, which then stays in the Infinity Cache.
-        warm_step = time_calls(lambda i: step(0))
-        warm_attn = time_calls(lambda i: attention(0))
-        warm_round = time_calls(lambda i: logit_round(0))
-        result["warm_cache"] = {
-            "note": "inputs resident in the 256 MB Infinity Cache (one input copy reused by every call); "
-                    "context only, the headline numbers above rotate copies past the cache",
-            "input_bytes": per_copy, "ms_per_step": round(warm_step, 5),
-            "attention_us": round(warm_attn * 1e3, 3),
-            "attention_gbps": round(work["attn_bytes"] / (warm_attn * 1e-3) / 1e9, 1),
-            "logit_round_us": round(warm_round * 1e3, 3)}
+    for k in ("attention_one_launch", "warm_cache"):
+        if k in m:
+            result[k] = m[k]
     if not args.no_overlap:
-        result["overlap"] = overlap_leg(lay, dev, args.steps, args.warmup, capture, time_calls,
-                                        (vout, dout, torch.as_tensor(lay.draft_row_indptr, device=dev)))
+        result["overlap"] = overlap_leg(lay, dev, args.steps, args.warmup, m["capture"], m["time_calls"],
+                                        (m["vout"], m["dout"], torch.as_tensor(lay.draft_row_indptr, device=dev)))
     if not args.no_block_sizing:
-        result["block_sizing"] = block_sizing_leg(lay, dev, time_calls)
+        result["block_sizing"] = block_sizing_leg(lay, dev, m["time_calls"])
     if not args.no_cpu_baseline:
-        host = {k: base[k] for k in ("q", "k_cache", "v_cache", "verify_logits", "draft_logits", "draft_tokens")}
-        sec, runs, threads, cores, split = cpu_baseline(lay, host, args.cpu_budget)
-        cpu_gbps = step_bytes / sec / 1e9
-        result["cpu_baseline"] = {"value": round(100.0 * cpu_gbps / HBM_PEAK_GBPS, 6),
-                                  "unit": result["unit"], "cores": threads, "kind": "oracle",
-                                  "ms_per_step": round(sec * 1e3, 2), "visible_cores": cores, **split,
-                                  "sample": f"{runs} whole step(s) of the same workload (all requests, heads "
-                                            f"and rows), fp64 numpy oracle, mean time per step"}
+        cb = cpu_baseline(lay, m["host_inputs"], args.cpu_budget)
+        cpu_gbps = step_bytes / cb["step_s"] / 1e9
+        result["cpu_baseline"] = {"value": round(100.0 * cpu_gbps / HBM_PEAK_GBPS, 6), "unit": result["unit"],
+                                  "cores": cb["blas_threads"], "kind": "oracle",
+                                  "ms_per_step": round(cb["step_s"] * 1e3, 2),
+                                  "cores_note": "threads of the BLAS library the oracle's matrix products ran on; "
+                                                "the rest of the oracle is single-threaded Python",
+                                  **{k: cb[k] for k in ("blas_threads", "visible_cores", "oracle_attention_ms",
+                                                        "oracle_accept_ms", "oracle_confidence_ms",
+                                                        "requests_timed", "sample")}}
         if not args.no_overlap or not args.no_block_sizing:
-            result["cpu_baseline"]["beside_next_rows"] = cpu_baseline_rows(lay, min(4.0, args.cpu_budget / 3))
+            result["cpu_baseline"]["beside_next_rows"] = cpu_baseline_rows(lay, dev, min(4.0, args.cpu_budget / 3))
+    headline_summary = m["summary"]
+    del m
+    torch.cuda.empty_cache()
+    if not args.no_all_configs:
+        # Every configuration timed the same way in the same run (summary
+        # figures; the headline above is the one named in `config.workload`).
+        allc = {}
+        for name in W_CONFIGS:
+            if name == args.workload:
+                allc[name] = headline_summary
+                continue
+            r = measure_workload(name, args.seed, dev, args.steps, args.warmup)
+            allc[name] = r["summary"]
+            del r
+            torch.cuda.empty_cache()
+        result["all_configs"] = allc
+    result["bench_wall_s"] = round(time.perf_counter() - t_start, 1)
     print(json.dumps(result), flush=True)
     return 0
+
+
+W_CONFIGS = ("tiny", "low", "mid", "high", "long")
 
 
 if __name__ == "__main__":

@@ -50,12 +50,15 @@ def test_attention_bytes_read_each_key_once():
 
 
 def test_traffic_record_reported_only_for_its_workload_and_source():
-    text = open(bench.TRAFFIC_FILE).read()
-    rec = json.loads(re.search(r"TRAFFIC_JSON (\{.*\})", text).group(1))
-    if rec["source_sha256"] == bench.attention_source_hash():
-        assert bench.measured_traffic(rec["workload"]) == rec["hbm_bytes_per_call"]
-    else:
-        assert bench.measured_traffic(rec["workload"]) is None
+    recs = bench.traffic_records()
+    assert recs
+    h = bench.attention_source_hash()
+    for rec in recs:
+        current = [r for r in recs if r["workload"] == rec["workload"] and r["source_sha256"] == h]
+        if current:
+            assert bench.measured_traffic(rec["workload"]) == current[0]["hbm_bytes_per_call"]
+        else:
+            assert bench.measured_traffic(rec["workload"]) is None
     assert bench.measured_traffic("no-such-workload") is None
 
 
@@ -63,7 +66,18 @@ def test_cpu_baseline_reports_each_oracle_function():
     lay = W.make_layout("tiny", seed=0)
     inputs = W.make_attention_inputs(lay, "cpu")
     inputs.update(W.make_logit_inputs(lay, "cpu"))
-    sec, runs, threads, cores, split = bench.cpu_baseline(lay, inputs, 0.2)
-    assert runs >= 1 and threads >= 1 and cores >= 1
-    assert set(split) == {"oracle_attention_ms", "oracle_accept_ms", "oracle_confidence_ms"}
-    assert sum(split.values()) <= sec * 1e3 + 0.05
+    cb = bench.cpu_baseline(lay, inputs, 0.2)
+    assert cb["requests_timed"] >= 1 and cb["blas_threads"] >= 1 and cb["visible_cores"] >= 1
+    split = [cb[k] for k in ("oracle_attention_ms", "oracle_accept_ms", "oracle_confidence_ms")]
+    assert sum(split) <= cb["step_s"] * 1e3 + 0.05
+
+
+def test_cpu_baseline_samples_requests_and_scales_to_the_batch():
+    """A batch of several requests is timed request by request on a sample
+    and scaled by the number of requests."""
+    lay = W.make_layout("high", seed=0, num_requests=6, ctx=("uniform", 16, 64))
+    inputs = W.make_attention_inputs(lay, "cpu")
+    inputs.update(W.make_logit_inputs(lay, "cpu"))
+    cb = bench.cpu_baseline(lay, inputs, 0.0)
+    assert cb["requests_timed"] == 1 and cb["distinct_requests"] == 1
+    assert "x 6 requests" in cb["sample"]
