@@ -16,6 +16,9 @@
  *                              P_1st - P_2nd and entropy per draft row
  *                              (Sec. 4.1)
  *   rg_verify_and_confidence   the two logit passes above in one call
+ *   rg_verify_and_confidence_noalloc
+ *                              the same without a workspace, for callers that
+ *                              cannot allocate
  *
  * and, for the predictive draft-verify overlap (Sec. 5.1, served as in
  * Sec. 5.3):
@@ -41,9 +44,10 @@
  *   or write (hipMalloc / torch CUDA tensors); "host" pointers are read by
  *   the CPU during the call only and may be reused as soon as it returns.
  * - The caller owns every buffer, including the workspace.  The library
- *   allocates no device memory and keeps no mutable global state; calls on
- *   different streams are independent provided they use distinct workspaces
- *   and outputs.
+ *   allocates no device memory and keeps no mutable global state other than
+ *   the static scratch of rg_verify_and_confidence_noalloc (one array per
+ *   GPU, and its address per device); calls on different streams are
+ *   independent provided they use distinct workspaces and outputs.
  * - Every call validates its arguments on the host first.  On a validation
  *   error it returns the error code, enqueues nothing and leaves every output
  *   untouched.  Otherwise it enqueues its kernels on `stream` (a hipStream_t,
@@ -69,7 +73,7 @@
 extern "C" {
 #endif
 
-#define RG_ABI_VERSION 5
+#define RG_ABI_VERSION 6
 
 typedef int32_t rg_status;
 #define RG_OK 0
@@ -246,6 +250,32 @@ rg_status rg_verify_and_confidence(const uint16_t* verify_logits, int64_t verify
                                    float* row_entropy, float* accept_entropy, int32_t draft_rows,
                                    int32_t* top1, int32_t* top2, float* p1, float* p2, float* margin,
                                    float* entropy, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * rg_verify_and_confidence without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).  Arguments, outputs and results
+ * are exactly rg_verify_and_confidence's; the chunk states that call keeps in
+ * the caller's workspace go to a static device array of
+ * RG_NOALLOC_SCRATCH_BYTES bytes instead, of which every GPU the library runs
+ * on holds one copy until the process ends (its address is looked up once
+ * per device, on that device's first call).  No device memory is allocated
+ * and no allocating library routine is called.  A round whose workspace
+ * (rg_verify_and_confidence_workspace) would exceed the array returns
+ * RG_ERR_UNSUPPORTED before anything is enqueued: e.g. at vocabulary 128256
+ * up to about 6500 verify plus 6500 draft rows fit.  Nothing in the array has
+ * to start at zero.  All calls on one GPU share its array: two calls whose
+ * kernels may overlap (other streams, other threads) race on it and must be
+ * ordered by the caller.
+ */
+#define RG_NOALLOC_SCRATCH_BYTES (4u << 20)
+rg_status rg_verify_and_confidence_noalloc(const uint16_t* verify_logits, int64_t verify_stride,
+                                           const uint16_t* draft_logits, int64_t draft_stride, int32_t vocab,
+                                           int32_t num_requests, int32_t verify_rows, const int32_t* row_indptr,
+                                           const int32_t* draft_tokens, int32_t* row_argmax, int32_t* accept_len,
+                                           int32_t* next_token, float* row_entropy, float* accept_entropy,
+                                           int32_t draft_rows, int32_t* top1, int32_t* top2, float* p1, float* p2,
+                                           float* margin, float* entropy, void* stream);
 
 /* ------------------------------------------------------------------------
  * Predictive draft-verify overlap (Sec. 5.1, Sec. 5.3)

@@ -22,6 +22,7 @@ import torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librecguide.so")
 
 RG_OK = 0
+NOALLOC_SCRATCH_BYTES = 4 << 20  # RG_NOALLOC_SCRATCH_BYTES
 _STATUS = {0: "ok", 1: "RG_ERR_NULL", 2: "RG_ERR_SHAPE", 3: "RG_ERR_UNSUPPORTED",
            4: "RG_ERR_WORKSPACE", 5: "RG_ERR_HIP"}
 
@@ -65,6 +66,7 @@ EXPORTS = ("rg_abi_version", "rg_status_string", "rg_draft_verify_attention_work
            "rg_draft_verify_attention", "rg_draft_verify_attention_plan",
            "rg_verify_accept_workspace", "rg_verify_accept", "rg_draft_confidence_workspace",
            "rg_draft_confidence", "rg_verify_and_confidence_workspace", "rg_verify_and_confidence",
+           "rg_verify_and_confidence_noalloc",
            "rg_multibranch_attention_workspace", "rg_multibranch_attention", "rg_plan_branches",
            "rg_match_branches", "rg_plan_block_sizes")
 
@@ -92,6 +94,8 @@ def _lib():
         "rg_verify_and_confidence_workspace": (I32, [I32, I32, I32, I32, ctypes.POINTER(SZ)]),
         "rg_verify_and_confidence": (I32, [P, I64, P, I64, I32, I32, I32, P, P, P, P, P, P, P,
                                            I32, P, P, P, P, P, P, P, SZ, P]),
+        "rg_verify_and_confidence_noalloc": (I32, [P, I64, P, I64, I32, I32, I32, P, P, P, P, P, P, P,
+                                                   I32, P, P, P, P, P, P, P]),
         "rg_multibranch_attention_workspace": (I32, [ctypes.POINTER(AttnLayout), ctypes.POINTER(BranchLayout),
                                                      ctypes.POINTER(SZ)]),
         "rg_multibranch_attention": (I32, [ctypes.POINTER(AttnLayout), ctypes.POINTER(BranchLayout),
@@ -488,10 +492,13 @@ def verify_and_confidence_workspace_bytes(num_requests: int, verify_rows: int, d
 def verify_and_confidence(verify_logits: torch.Tensor, row_indptr: torch.Tensor, draft_tokens: torch.Tensor,
                           draft_logits: torch.Tensor, *, workspace: Optional[torch.Tensor] = None,
                           out_verify: Optional[Dict[str, torch.Tensor]] = None,
-                          out_draft: Optional[Dict[str, torch.Tensor]] = None,
+                          out_draft: Optional[Dict[str, torch.Tensor]] = None, noalloc: bool = False,
                           stream=None) -> Tuple[Dict[str, torch.Tensor], Dict[str, torch.Tensor]]:
     """Both logit passes of a round in one call (rg_verify_and_confidence):
-    returns the outputs of verify_accept and of draft_confidence."""
+    returns the outputs of verify_accept and of draft_confidence.  With
+    ``noalloc`` the allocation-free variant runs instead
+    (rg_verify_and_confidence_noalloc: the library's static scratch, no
+    workspace; ``workspace`` is ignored)."""
     for t, name in ((verify_logits, "verify_logits"), (draft_logits, "draft_logits")):
         if not t.is_cuda or t.dtype != torch.bfloat16 or t.dim() != 2 or t.stride(1) != 1:
             raise TypeError(f"{name} must be a CUDA bf16 [rows, vocab] tensor with unit column stride")
@@ -514,18 +521,20 @@ def verify_and_confidence(verify_logits: torch.Tensor, row_indptr: torch.Tensor,
     for k, dt in (("top1", torch.int32), ("top2", torch.int32), ("p1", torch.float32), ("p2", torch.float32),
                   ("margin", torch.float32), ("entropy", torch.float32)):
         od.setdefault(k, torch.empty(drows, dtype=dt, device=dev))
+    args = (verify_logits.data_ptr() if vrows else None, verify_logits.stride(0) if vrows else vocab,
+            draft_logits.data_ptr() if drows else None, draft_logits.stride(0) if drows else vocab, vocab, R, vrows,
+            row_indptr.data_ptr(), draft_tokens.data_ptr() if vrows else None,
+            ov["row_argmax"].data_ptr() if vrows else None, ov["accept_len"].data_ptr(), ov["next_token"].data_ptr(),
+            _ptr(ov.get("row_entropy")) if vrows else None, _ptr(ov.get("accept_entropy")), drows,
+            _ptr(od["top1"]) if drows else None, _ptr(od["top2"]) if drows else None,
+            _ptr(od["p1"]) if drows else None, _ptr(od["p2"]) if drows else None,
+            _ptr(od.get("margin")) if drows else None, _ptr(od.get("entropy")) if drows else None)
+    if noalloc:
+        _check(_lib().rg_verify_and_confidence_noalloc(*args, _stream(stream)), "rg_verify_and_confidence_noalloc")
+        return ov, od
     if workspace is None:
         workspace = new_workspace(verify_and_confidence_workspace_bytes(R, vrows, drows, vocab), dev)
-    st = _lib().rg_verify_and_confidence(
-        verify_logits.data_ptr() if vrows else None, verify_logits.stride(0) if vrows else vocab,
-        draft_logits.data_ptr() if drows else None, draft_logits.stride(0) if drows else vocab, vocab, R, vrows,
-        row_indptr.data_ptr(), draft_tokens.data_ptr() if vrows else None,
-        ov["row_argmax"].data_ptr() if vrows else None, ov["accept_len"].data_ptr(), ov["next_token"].data_ptr(),
-        _ptr(ov.get("row_entropy")) if vrows else None, _ptr(ov.get("accept_entropy")), drows,
-        _ptr(od["top1"]) if drows else None, _ptr(od["top2"]) if drows else None,
-        _ptr(od["p1"]) if drows else None, _ptr(od["p2"]) if drows else None,
-        _ptr(od.get("margin")) if drows else None, _ptr(od.get("entropy")) if drows else None,
-        workspace.data_ptr(), workspace.numel(), _stream(stream))
+    st = _lib().rg_verify_and_confidence(*args, workspace.data_ptr(), workspace.numel(), _stream(stream))
     _check(st, "rg_verify_and_confidence")
     return ov, od
 

@@ -19,6 +19,7 @@ static_assert(RG_BLOCK_MAX_CANDIDATES == rg::kMaxBlockCandidates, "header and ke
 static_assert(RG_BLOCK_MAX_S_BINS == rg::kMaxSBins, "header and kernel limits agree");
 static_assert(RG_BLOCK_MAX_REQUESTS == rg::kMaxBucketRequests, "header and kernel limits agree");
 static_assert(RG_BRANCH_MAX_REQS_PER_LAUNCH == rg::kMaxReqPerLaunchBr, "header and kernel limits agree");
+static_assert(RG_NOALLOC_SCRATCH_BYTES == rg::kNoAllocScratchBytes, "header and scratch size agree");
 
 namespace {
 
@@ -596,6 +597,26 @@ rg_status rg_verify_and_confidence(const uint16_t* verify_logits, int64_t verify
   return launch_round(v, d, static_cast<hipStream_t>(stream)) == hipSuccess ? RG_OK : RG_ERR_HIP;
 }
 
+rg_status rg_verify_and_confidence_noalloc(const uint16_t* verify_logits, int64_t verify_stride,
+                                           const uint16_t* draft_logits, int64_t draft_stride, int32_t vocab,
+                                           int32_t num_requests, int32_t verify_rows, const int32_t* row_indptr,
+                                           const int32_t* draft_tokens, int32_t* row_argmax, int32_t* accept_len,
+                                           int32_t* next_token, float* row_entropy, float* accept_entropy,
+                                           int32_t draft_rows, int32_t* top1, int32_t* top2, float* p1, float* p2,
+                                           float* margin, float* entropy, void* stream) {
+  // The same workspace layout as rg_verify_and_confidence, carved from the
+  // static scratch: sizes past it are refused before anything is looked up.
+  size_t need = 0;
+  const rg_status st = rg_verify_and_confidence_workspace(num_requests, verify_rows, draft_rows, vocab, &need);
+  if (st != RG_OK) return st;
+  if (need > kNoAllocScratchBytes) return RG_ERR_UNSUPPORTED;
+  void* ws = nullptr;
+  if (need > 0 && noalloc_scratch(&ws) != hipSuccess) return RG_ERR_HIP;
+  return rg_verify_and_confidence(verify_logits, verify_stride, draft_logits, draft_stride, vocab, num_requests,
+                                  verify_rows, row_indptr, draft_tokens, row_argmax, accept_len, next_token,
+                                  row_entropy, accept_entropy, draft_rows, top1, top2, p1, p2, margin, entropy,
+                                  ws, need, stream);
+}
 
 rg_status rg_plan_branches(const float* margin, const int32_t* top2, const int32_t* row_indptr,
                            int32_t num_requests, int32_t total_rows, float delta, int32_t* n_risky,

@@ -25,6 +25,8 @@
 // mismatch.  The kernel boundary is the
 // only cross-work-group synchronisation: no atomics, no device-scope fences,
 // and the workspace needs no initialisation.
+#include <mutex>
+
 #include "rg_internal.h"
 
 namespace rg {
@@ -586,7 +588,37 @@ int draft_finalize_groups(const DraftArgs& a) {
   return (a.rows + rows_per_group - 1) / rows_per_group;
 }
 
+// Scratch of the allocation-free logit round (rg_verify_and_confidence_noalloc):
+// the chunk states that rg_verify_and_confidence keeps in its caller's
+// workspace.  Every GPU the library runs on holds one copy until the process
+// ends; the row passes write every state the finalize pass reads, so nothing
+// in it has to start at zero.
+__device__ __attribute__((aligned(256))) unsigned char scratch[kNoAllocScratchBytes];
+
 }  // namespace
+
+// Device address of this GPU's copy of `scratch`, looked up once per device
+// (with that device current) and kept: in host code the array's name is only
+// a host-side stand-in, never a device address.
+hipError_t noalloc_scratch(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
   if (a.grid_rows > 0) {

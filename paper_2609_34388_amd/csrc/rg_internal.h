@@ -137,6 +137,11 @@ hipError_t launch_draft(const DraftArgs& a, hipStream_t stream);
 // Verify and draft passes of one round together: two launches in all.
 hipError_t launch_round(const VerifyArgs& v, const DraftArgs& d, hipStream_t stream);
 
+// Static device scratch of the allocation-free logit round (logits.hip):
+// its size, and this device's address of it (looked up on first use).
+constexpr size_t kNoAllocScratchBytes = size_t(4) << 20;  // equals RG_NOALLOC_SCRATCH_BYTES
+hipError_t noalloc_scratch(void** ptr);
+
 // Branch planning and matching (branches.hip).
 struct PlanBranchArgs {
   const float* margin;
