@@ -13,20 +13,20 @@
 // so every K/V byte of a chunk is read from HBM once for all of them.  The 8
 // compute waves of a work group split the group into 32-column tiles and,
 // when there are fewer than 8 tiles, the chunk's 32-key sub-tiles into key
-// groups; 4 more waves only issue the copies into LDS.
+// groups; 4 more waves only copy K and V into LDS.
 // Requests whose keys span several chunks write normalised partial outputs
 // plus (max, sum) per column; a second kernel merges them with the usual
 // log-sum-exp weights (or, in the opt-in one-launch mode, merge items of the
 // same launch, taken from a work queue once the chunks they merge are done).
 //
-// K and V of 128 keys (8 pages) at a time are copied straight into LDS
-// (three K buffers and two V buffers: the next buffer's copies, and with
-// several key groups also the K after it, are in flight while the current
-// one is computed).  On each 32-key sub-tile a wave forms S^T = K Q^T with
-// v_mfma_f32_32x32x16_bf16 (K rows are the MFMA rows, query columns the MFMA
-// columns), applies the mask, updates the running max and sum in fp32 (exp2
-// with the scale folded in), converts P to bf16 and accumulates
-// O^T += V^T P^T with the same MFMA.  The K rows of a sub-tile are loaded in a
+// K and V of 128 keys (8 pages) at a time pass through LDS (two slots each):
+// the copy waves load the next two buffers into registers with ordinary
+// vector loads while the current one is computed, and write each to its LDS
+// slot just before its barrier.  On each 32-key sub-tile a wave forms
+// S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (K rows are the MFMA rows, query
+// columns the MFMA columns), applies the mask, updates the running max and
+// sum in fp32 (exp2 with the scale folded in), converts P to bf16 and
+// accumulates O^T += V^T P^T with the same MFMA.  The K rows of a sub-tile are loaded in a
 // permuted order (bits 2 and 3 of the row index swapped) so that the S^T
 // accumulator registers a lane holds are exactly the P^T operand the PV MFMA
 // needs and the matching V^T operand is 8 consecutive keys of one head
@@ -36,6 +36,8 @@
 // pool, unused slots of a request's last page included); buffer rows past
 // the chunk end get their scores masked to -inf and their values zeroed, so
 // whatever those slots hold (NaN included) never reaches the output.
+#include <type_traits>
+
 #include "rg_internal.h"
 
 namespace rg {
@@ -85,27 +87,10 @@ __device__ __forceinline__ int xcd_item(int grid_items) {
   return (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
 }
 
-// Direct global -> LDS copy of 16 bytes per lane (LDS-DMA).  The wave's 64
-// lanes fill 1 KiB of LDS starting at `lds_byte_addr` (lane L at +16 L); the
-// source is a wave-uniform 64-bit base in SGPRs plus a per-lane 32-bit byte
-// offset.  Issued through inline assembly so that the compiler does not
-// insert a wait for every outstanding copy before each LDS read; the kernel
-// waits on the vector-memory counter itself.  m0 is saved and restored.
-__device__ __forceinline__ void dma16_s(const void* sbase, uint32_t voff, uint32_t lds_byte_addr) {
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %1\n\t"
-      "global_load_lds_dwordx4 %2, %3\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(__builtin_amdgcn_readfirstlane(lds_byte_addr)), "v"(voff), "s"(sbase)
-      : "memory");
-}
-
 // Work-group barrier that orders LDS only.  __syncthreads() also fences
 // global memory, which makes every wave wait for all of its outstanding
-// vector-memory operations -- the whole LDS-DMA ring -- at each barrier.
+// vector-memory operations -- the copy waves' loads of the next buffers --
+// at each barrier.
 __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
@@ -152,8 +137,9 @@ constexpr int kWaves = 8;      // compute waves per work group (two per SIMD)
 constexpr int kProducers = 4;  // copy waves per work group (one per SIMD)
 constexpr int kThreads = 64 * (kWaves + kProducers);
 constexpr int kSuper = 128;  // keys staged per LDS buffer (four 32-key sub-tiles)
-constexpr int kKBufs = 3;    // K buffers: one computed, two being filled
+constexpr int kKBufs = 2;    // K buffers: one computed, one being filled
 constexpr int kVBufs = 2;    // V buffers: one computed, one being filled
+static_assert(kKBufs == 2 && kVBufs == 2, "two copy-wave pairs, one per buffer parity and LDS slot");
 static_assert(kSuper % kKeyTile == 0, "a super-tile is a whole number of key tiles");
 
 // Work group = 8 compute waves over (column tiles) x (key groups).  A
@@ -164,10 +150,14 @@ static_assert(kSuper % kKeyTile == 0, "a super-tile is a whole number of key til
 // through LDS at the end.
 //
 // Keys stream through LDS 128 at a time (K and V of 8 pages), one barrier per
-// 128 keys.  The copies are issued by 4 dedicated waves (one per SIMD): a CU
-// accepts a 1 KiB LDS-DMA instruction only every few dozen cycles, and a
-// compute wave issuing its share would stall for most of a buffer's worth of
-// them instead of computing.
+// 128 keys.  The copies are made by 4 dedicated waves (one per SIMD), two per
+// buffer parity, each holding its share of a buffer (32 KiB per pair) in
+// registers from its load until just before that buffer's barrier: two
+// buffers are in flight from HBM, and the compute waves spend no issue slots
+// or registers on copies.  (Loads straight into LDS, which need no staging
+// registers, measured slower: a CU takes such a 1 KiB load only every few
+// dozen cycles, about 5.9 TB/s over the chip against about 7.1 TB/s for
+// plain vector loads.)
 //
 // PERSIST: the item runs inside the one-launch work-queue kernel.  Every wave
 // then passes the same barriers (the copy waves join the key-group merge),
@@ -180,18 +170,17 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
   constexpr int KSTEPS = D / 16;               // MFMA k-steps of q.k
   constexpr int DT = D / 32;                   // 32-wide head-dim tiles of the output
   constexpr int SUPER = kSuper * D;            // bf16 elements of one K (or V) buffer
-  constexpr int BLOCKS = SUPER * 2 / 1024;     // 1 KiB DMA blocks per K (or V) buffer
+  constexpr int BLOCKS = SUPER * 2 / 1024;     // 1 KiB copy blocks per K (or V) buffer
   constexpr int KPB = 1024 / (2 * D);          // keys per K block
   constexpr int VBPP = D / 32;                 // V blocks per page
-  constexpr int GP = 2 * BLOCKS / kProducers;  // DMA instructions per copy wave per buffer
   constexpr int COLS = 32 * kWaves;            // columns per column group
-  static_assert(2 * BLOCKS % kProducers == 0 && BLOCKS == kProducers * (GP / 2), "DMA blocks split evenly");
-  static_assert((kKBufs + kVBufs) * SUPER * 2 >= kWaves * (64 * 16 * DT + 128) * 4, "merge area");
+  // key-group merge: one slot per wave that hands its state over (every such wave has index >= 1)
+  static_assert((kKBufs + kVBufs) * SUPER * 2 >= (kWaves - 1) * (64 * 16 * DT + 128) * 4, "merge area");
 
   // kbuf[b] = K of 128 keys ([key][D], 16-byte chunks swizzled per row),
   // vbuf[b] = V of 8 pages ([page][D][16 keys], halves swizzled per row).
-  // K runs two buffers ahead and V one: a buffer's K is issued a whole
-  // buffer period before it is needed, with 160 KiB of LDS in all.
+  // Two slots of each (128 KiB of LDS at D = 128): buffer s in slot s % 2
+  // while buffer s + 1 is written into the other.
   auto kbuf = [&](int s) { return lds + (s % kKBufs) * SUPER; };
   auto vbuf = [&](int s) { return lds + (kKBufs + s % kVBufs) * SUPER; };
 
@@ -223,6 +212,130 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
   // no SIMD carries two whole tiles while another idles.
   const int nct = min(kWaves, (M - cg * COLS + 31) / 32);
   const bool producer = wave >= kWaves;  // wave-uniform: copy wave
+  // Pages of this chunk: entries pg0 .. pg0 + npg - 1 of the request's list.
+  const int pg0 = kbeg / kPageSize;
+  const int npg = (kend + kPageSize - 1) / kPageSize - pg0;
+  // The copy waves read page numbers through the scalar cache (uniform
+  // addresses in the constant address space): no LDS stage, no barrier.
+  typedef const int32_t __attribute__((address_space(4))) * cpage_ptr;
+  const cpage_ptr chunk_pages = (cpage_ptr)(a.page_indices + rq.page_start + pg0);
+
+  const size_t head_stride = (size_t)kPageSize * D;  // elements per (page, head)
+  const char* kbase_g = reinterpret_cast<const char*>(a.k_cache + (size_t)hk * head_stride);
+  const char* vbase_g = reinterpret_cast<const char*>(a.v_cache + (size_t)hk * head_stride);
+  const size_t page_bytes = (size_t)a.hkv * head_stride * 2;
+
+  // Copy waves.  The four copy waves form two pairs, one per buffer parity:
+  // pair `par` copies buffers par, par + 2, ... into LDS slot par.  Wave q of
+  // the pair moves K blocks b = q + 2 i and V blocks b = q + 2 i of its
+  // buffer (i = 0 .. NB - 1): a K block is KPB keys, a V block 32 head dims of
+  // one page, 1 KiB each; lane L's 16 bytes of a block go to byte 16 L of the
+  // block's place in the slot.  A wave reads its buffer's 8 page numbers
+  // (one batch of scalar loads), loads its blocks into registers and writes
+  // them to LDS before the buffer's barrier.  Page slots past the chunk's
+  // last page repeat that page, so buffer rows past the chunk end hold other
+  // tokens or unused slots of the last page (memory of the pool either way);
+  // their scores are masked and their values zeroed before use.
+  constexpr int WPG = kProducers / 2;  // copy waves per parity
+  constexpr int NB = BLOCKS / WPG;     // K (and V) blocks per copy wave and buffer
+  static_assert(BLOCKS % WPG == 0 && NB % 2 == 0, "blocks split evenly over a pair");
+  const int pw = wave - kWaves;
+  const int par = pw / WPG;  // wave-uniform: buffer parity (and LDS slot) of this copy wave
+  const int q = pw % WPG;
+  auto read_pages = [&](int s, int (&pg)[kSuper / kPageSize]) {
+    const int base = s * (kSuper / kPageSize);
+#pragma unroll
+    for (int j = 0; j < kSuper / kPageSize; ++j) pg[j] = chunk_pages[min(base + j, npg - 1)];
+  };
+  // A lane's byte offset inside its page repeats with period 2 in i: blocks
+  // i and i + 2 lie 2 WPG = 4 blocks apart, 4 KPB keys (a multiple of 16,
+  // so the same page slot and the same swap23 row bits) or 4 V blocks (a
+  // multiple of VBPP, so the same head dims).
+  static_assert((2 * WPG * KPB) % kPageSize == 0 && (2 * WPG) % VBPP == 0, "offsets repeat every two blocks");
+  uint32_t koff[2], voff[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int b = q + WPG * e;
+    const int kk = b * KPB + lane / NCH;
+    koff[e] = (uint32_t)((((kk % kPageSize) * D) + (((lane % NCH) ^ (swap23(kk & 31) & (NCH - 1))) * 8)) * 2);
+    const int d = (b % VBPP) * 32 + (lane >> 1);
+    voff[e] = (uint32_t)((d * kPageSize + ((lane & 1) ^ vswz(d)) * 8) * 2);
+  }
+  // This wave's blocks of one buffer: NB K blocks, then NB V blocks.
+  auto load_set = [&](const int (&pg)[kSuper / kPageSize], u32x4 (&r)[2 * NB]) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int b = q + WPG * i;
+      r[i] = __builtin_nontemporal_load(
+          (const u32x4*)(kbase_g + (size_t)pg[(b * KPB) / kPageSize] * page_bytes + koff[i & 1]));
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int b = q + WPG * i;
+      r[NB + i] = __builtin_nontemporal_load((const u32x4*)(vbase_g + (size_t)pg[b / VBPP] * page_bytes + voff[i & 1]));
+    }
+  };
+  auto store_set = [&](const u32x4 (&r)[2 * NB]) {
+    uint16_t* kd = lds + par * SUPER + q * 512 + lane * 8;
+    uint16_t* vd = lds + (kKBufs + par) * SUPER + q * 512 + lane * 8;
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      *(u32x4*)(kd + i * WPG * 512) = r[i];
+      *(u32x4*)(vd + i * WPG * 512) = r[NB + i];
+    }
+  };
+
+  const int nsup = (kend - kbeg + kSuper - 1) / kSuper;
+  // Zero the values of keys past the chunk end in the last buffer (every
+  // wave takes part, so both loops below pass the same barriers), by 16-byte
+  // units (page slot pp, head dim d, half h = keys 16 pp + 8 h ..).
+  auto tail_fixup = [&](int s, int nvalid) {
+    uint16_t* vz = vbuf(s);
+    for (int u = tid; u < (kSuper / kPageSize) * D * 2; u += kThreads) {
+      const int pp = u / (2 * D), d = (u >> 1) % D, h = u & 1;
+      const int kfirst = kPageSize * pp + 8 * h;
+      if (kfirst + 8 <= nvalid) continue;
+      uint16_t* unit = vz + pp * (D * kPageSize) + d * kPageSize + ((h ^ vswz(d)) * 8);
+      if (kfirst >= nvalid) {
+        *(u32x4*)unit = u32x4{0u, 0u, 0u, 0u};
+      } else {
+        for (int e = nvalid - kfirst; e < 8; ++e) unit[e] = 0;
+      }
+    }
+    lds_barrier();
+  };
+
+  if (producer) {
+    // Buffer s's loads go out after barrier s - 2 (buffers 0 and 1 at the
+    // start) and land in LDS slot s % 2 before barrier s -- over buffer
+    // s - 2, computed before barrier s - 1 -- so two buffers are in flight
+    // per work group, one per pair, and each wave waits only for its own.
+    // The page numbers come from the scalar cache just before the loads.
+    u32x4 r[2 * NB];
+    int pg[kSuper / kPageSize];
+    if (par < nsup) {
+      read_pages(par, pg);
+      load_set(pg, r);
+    }
+    for (int s = 0; s < nsup; ++s) {
+      const bool mine = (s & 1) == par;
+      if (mine) store_set(r);
+      lds_barrier();  // everyone's copies of buffer s are in; buffers of s - 1 are no longer read
+      const int nvalid = kend - (kbeg + s * kSuper);
+      if (nvalid < kSuper) tail_fixup(s, nvalid);
+      if (mine && s + 2 < nsup) {
+        read_pages(s + 2, pg);
+        load_set(pg, r);
+      }
+    }
+    if constexpr (PERSIST) {
+      if (nct < 8) {  // the key-group merge's two barriers
+        lds_barrier();
+        lds_barrier();
+      }
+    }
+    return;
+  }
   int ct, kg, kgi, kstride;
   if (nct <= 4) {
     const int nct2 = nct <= 1 ? 1 : nct <= 2 ? 2 : 4;
@@ -304,52 +417,6 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
   }
   int wave_min_lim = valid ? lim : kend;
   for (int off = 32; off >= 1; off >>= 1) wave_min_lim = min(wave_min_lim, __shfl_xor(wave_min_lim, off));
-
-  // Pages of this chunk: entries pg0 .. pg0 + npg - 1 of the request's list.
-  const int pg0 = kbeg / kPageSize;
-  const int npg = (kend + kPageSize - 1) / kPageSize - pg0;
-  // The copy waves read page numbers through the scalar cache (uniform
-  // addresses in the constant address space): no LDS stage, no barrier.
-  typedef const int32_t __attribute__((address_space(4))) * cpage_ptr;
-  const cpage_ptr chunk_pages = (cpage_ptr)(a.page_indices + rq.page_start + pg0);
-
-  const size_t head_stride = (size_t)kPageSize * D;  // elements per (page, head)
-  const char* kbase_g = reinterpret_cast<const char*>(a.k_cache + (size_t)hk * head_stride);
-  const char* vbase_g = reinterpret_cast<const char*>(a.v_cache + (size_t)hk * head_stride);
-  const size_t page_bytes = (size_t)a.hkv * head_stride * 2;
-
-  // Copy wave pw issues blocks b = pw + 4 i of each buffer's K (and of its
-  // V): KPB keys, or 32 head dims of one page, per 1 KiB block.  It reads the
-  // 8 page numbers of the buffer (one batch of scalar loads), then issues.
-  // Page slots past the chunk's last page repeat that page, so buffer rows
-  // past the chunk end hold other tokens or unused slots of the last page
-  // (memory of the pool either way); their scores are masked and their values
-  // zeroed before use.
-  const int pw = wave - kWaves;
-  auto read_pages = [&](int s, int (&pg)[kSuper / kPageSize]) {
-    const int base = s * (kSuper / kPageSize);
-#pragma unroll
-    for (int j = 0; j < kSuper / kPageSize; ++j) pg[j] = chunk_pages[min(base + j, npg - 1)];
-  };
-  auto issue_k = [&](int s, const int (&pg)[kSuper / kPageSize]) {
-#pragma unroll
-    for (int i = 0; i < GP / 2; ++i) {
-      const int b = pw + i * kProducers;  // wave-uniform
-      const int kk = b * KPB + lane / NCH;
-      const uint32_t off = (uint32_t)((((kk % kPageSize) * D) + (((lane % NCH) ^ (swap23(kk & 31) & (NCH - 1))) * 8)) * 2);
-      dma16_s(kbase_g + (size_t)pg[(b * KPB) / kPageSize] * page_bytes, off,
-              (uint32_t)(uintptr_t)(kbuf(s) + b * 512));
-    }
-  };
-  auto issue_v = [&](int s, const int (&pg)[kSuper / kPageSize]) {
-#pragma unroll
-    for (int i = 0; i < GP / 2; ++i) {
-      const int b = pw + i * kProducers;  // V block of the buffer
-      const int d = (b % VBPP) * 32 + (lane >> 1);
-      const uint32_t off = (uint32_t)((d * kPageSize + ((lane & 1) ^ vswz(d)) * 8) * 2);
-      dma16_s(vbase_g + (size_t)pg[b / VBPP] * page_bytes, off, (uint32_t)(uintptr_t)(vbuf(s) + b * 512));
-    }
-  };
 
   f32x16 acc[DT];
   for (int dt = 0; dt < DT; ++dt)
@@ -433,73 +500,6 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
     }
     __builtin_amdgcn_sched_barrier(0);  // keep the next sub-tile's loads after this one's PV
   };
-  const int nsup = (kend - kbeg + kSuper - 1) / kSuper;
-  // Zero the values of keys past the chunk end in the last buffer (every
-  // wave takes part, so both loops below pass the same barriers), by 16-byte
-  // units (page slot pp, head dim d, half h = keys 16 pp + 8 h ..).
-  auto tail_fixup = [&](int s, int nvalid) {
-    uint16_t* vz = vbuf(s);
-    for (int u = tid; u < (kSuper / kPageSize) * D * 2; u += kThreads) {
-      const int pp = u / (2 * D), d = (u >> 1) % D, h = u & 1;
-      const int kfirst = kPageSize * pp + 8 * h;
-      if (kfirst + 8 <= nvalid) continue;
-      uint16_t* unit = vz + pp * (D * kPageSize) + d * kPageSize + ((h ^ vswz(d)) * 8);
-      if (kfirst >= nvalid) {
-        *(u32x4*)unit = u32x4{0u, 0u, 0u, 0u};
-      } else {
-        for (int e = nvalid - kfirst; e < 8; ++e) unit[e] = 0;
-      }
-    }
-    lds_barrier();
-  };
-
-  if (producer) {
-    // Deep mode (key groups > 1, where compute is short and the copies set the
-    // pace): K runs two buffers ahead.  Issue order K(0), V(0), K(1); then at
-    // buffer s: V(s + 1), K(s + 2), so when V(s) is complete only K(s + 1) can
-    // still be out.  Otherwise K and V of s + 1 go out together at buffer s.
-    // The page numbers a buffer's copies need are read before the barrier
-    // that frees its LDS, so their load latency passes while the buffer
-    // being computed is still in use, not after it.
-    const bool deep = nct <= 4;  // every tile split over key groups
-    int pa[kSuper / kPageSize], pb[kSuper / kPageSize];
-    read_pages(0, pa);
-    issue_k(0, pa);
-    issue_v(0, pa);
-    if (deep && nsup > 1) {
-      read_pages(1, pb);
-      issue_k(1, pb);
-    }
-    for (int s = 0; s < nsup; ++s) {
-      // deep: V(s + 1) uses the pages of s + 1 (still in pb), K(s + 2) those of s + 2
-      if (deep) {
-        if (s + 2 < nsup) read_pages(s + 2, pa);
-      } else if (s + 1 < nsup) {
-        read_pages(s + 1, pa);
-      }
-      if (deep && s + 1 < nsup) wait_vmcnt<GP / 2>();  // this copy wave's K(s) and V(s)
-      else wait_vmcnt<0>();
-      lds_barrier();  // everyone's copies of buffer s are in; buffers of s - 1 are no longer read
-      const int nvalid = kend - (kbeg + s * kSuper);
-      if (nvalid < kSuper) tail_fixup(s, nvalid);
-      if (deep) {
-        if (s + 1 < nsup) issue_v(s + 1, pb);  // into the V buffer of s - 1
-        if (s + 2 < nsup) issue_k(s + 2, pa);  // into the K buffer of s - 1
-#pragma unroll
-        for (int j = 0; j < kSuper / kPageSize; ++j) pb[j] = pa[j];
-      } else if (s + 1 < nsup) {
-        issue_k(s + 1, pa);  // into the K buffer of s - 2
-        issue_v(s + 1, pa);  // into the V buffer of s - 1
-      }
-    }
-    if constexpr (PERSIST) {
-      if (nct < 8) {  // the key-group merge's two barriers
-        lds_barrier();
-        lds_barrier();
-      }
-    }
-    return;
-  }
   for (int s = 0; s < nsup; ++s) {
     lds_barrier();
     const int k0 = kbeg + s * kSuper;
@@ -523,7 +523,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
     float* area = reinterpret_cast<float*>(lds);
     constexpr int PER = 64 * 16 * DT + 128;  // floats per wave slot
     if (tile_on && kgi > 0) {
-      float* slot = area + wave * PER;
+      float* slot = area + (wave - 1) * PER;
       for (int dt = 0; dt < DT; ++dt)
         for (int ib = 0; ib < 4; ++ib)
           *(float4*)(slot + ((dt * 4 + ib) * 64 + lane) * 4) =
@@ -534,7 +534,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
     lds_barrier();
     if (!tile_on || kgi > 0) return;
     for (int k = 1; k < kg; ++k) {
-      const float* slot = area + (wave + k * kstride) * PER;
+      const float* slot = area + (wave + k * kstride - 1) * PER;
       const float mk = slot[64 * 16 * DT + lane];
       if (mk == kNegInf) continue;
       const float lk = slot[64 * 16 * DT + 64 + lane];
@@ -801,7 +801,7 @@ __global__ __launch_bounds__(kThreads) void attn_persist_kernel(AttnArgs a, Plan
   int* const s_next = reinterpret_cast<int*>(lds) + WORDS - 1;
   static_assert(kCombRowsPersist * kCombPartsPersist == kThreads, "combine items use the whole work group");
   static_assert((kCombPartsPersist - 1) * 10 * kCombRowsPersist < WORDS - 1, "combine exchange below the slot");
-  static_assert(kWaves * (64 * 16 * (D / 32) + 128) < WORDS - 1, "key-group merge area below the slot");
+  static_assert((kWaves - 1) * (64 * 16 * (D / 32) + 128) < WORDS - 1, "key-group merge area below the slot");
   const int total = p.total_items + p.total_comb;
   const int grid = p.persist_grid;
   // First item: the work group's index, which the queue head then continues
