@@ -475,7 +475,7 @@ rg_status make_verify_args(const uint16_t* logits, int64_t row_stride, int32_t v
   if (!row_indptr || !accept_len || !next_token) return RG_ERR_NULL;
   if (total_rows > 0 && (!logits || !draft_tokens || !row_argmax)) return RG_ERR_NULL;
   if (row_stride < vocab) return RG_ERR_SHAPE;
-  if ((int64_t)total_rows * logit_chunks(vocab) > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
+  if (((int64_t)total_rows << logit_chunk_shift(vocab)) > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
   const size_t need = verify_ws_bytes(total_rows, vocab);
   if (total_rows > 0 && (ws == nullptr || ws_bytes < need || !aligned(ws, 16))) return RG_ERR_WORKSPACE;
   std::memset(&a, 0, sizeof(a));
@@ -485,6 +485,7 @@ rg_status make_verify_args(const uint16_t* logits, int64_t row_stride, int32_t v
   a.num_req = num_requests;
   a.rows = total_rows;
   a.nchunk = logit_chunks(vocab);
+  a.cshift = logit_chunk_shift(vocab);
   a.row_indptr = row_indptr;
   a.tokens = draft_tokens;
   a.row_argmax = row_argmax;
@@ -494,7 +495,7 @@ rg_status make_verify_args(const uint16_t* logits, int64_t row_stride, int32_t v
   a.accept_entropy = accept_entropy;
   a.chunk_st = static_cast<float4*>(ws);
   a.vec = (aligned(logits, 16) && row_stride % 8 == 0) ? 1 : 0;
-  a.grid_rows = (int32_t)round_up((int64_t)total_rows * a.nchunk, 8);
+  a.grid_rows = (int32_t)round_up((int64_t)total_rows << a.cshift, 8);
   return RG_OK;
 }
 
@@ -504,7 +505,7 @@ rg_status make_draft_args(const uint16_t* logits, int64_t row_stride, int32_t vo
   if (total_rows < 0 || vocab < 2) return RG_ERR_SHAPE;
   if (total_rows > 0 && (!logits || !top1 || !top2 || !p1 || !p2)) return RG_ERR_NULL;
   if (row_stride < vocab) return RG_ERR_SHAPE;
-  if ((int64_t)total_rows * logit_chunks(vocab) > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
+  if (((int64_t)total_rows << logit_chunk_shift(vocab)) > INT32_MAX / 2) return RG_ERR_UNSUPPORTED;
   const size_t need = draft_ws_bytes(total_rows, vocab);
   if (total_rows > 0 && (ws == nullptr || ws_bytes < need || !aligned(ws, 16))) return RG_ERR_WORKSPACE;
   std::memset(&a, 0, sizeof(a));
@@ -513,6 +514,7 @@ rg_status make_draft_args(const uint16_t* logits, int64_t row_stride, int32_t vo
   a.vocab = vocab;
   a.rows = total_rows;
   a.nchunk = logit_chunks(vocab);
+  a.cshift = logit_chunk_shift(vocab);
   a.top1 = top1;
   a.top2 = top2;
   a.p1 = p1;
@@ -524,7 +526,7 @@ rg_status make_draft_args(const uint16_t* logits, int64_t row_stride, int32_t vo
   if (w != nullptr) w += align256((size_t)total_rows * a.nchunk * 16);
   a.chunk_b = reinterpret_cast<float2*>(w);
   a.vec = (aligned(logits, 16) && row_stride % 8 == 0) ? 1 : 0;
-  a.grid_rows = (int32_t)round_up((int64_t)total_rows * a.nchunk, 8);
+  a.grid_rows = (int32_t)round_up((int64_t)total_rows << a.cshift, 8);
   return RG_OK;
 }
 

@@ -147,10 +147,12 @@ __device__ __forceinline__ T wave_reduce(T v, Op op) {
   return op(op(lane_read(v, 0), lane_read(v, 16)), op(lane_read(v, 32), lane_read(v, 48)));
 }
 
-// Largest and second largest value of the multiset {a1 >= a2} U {b1 >= b2}.
+// Largest and second largest value of the multiset {a1 >= a2} U {b1 >= b2}:
+// the runner-up is max(min(a1, b1), max(a2, b2)), which is the median of
+// a1, b1 and max(a2, b2) (that maximum is at most max(a1, b1)).
 __device__ __forceinline__ void top2_merge(float& a1, float& a2, float b1, float b2) {
-  a2 = fmaxf(fminf(a1, b1), fmaxf(a2, b2));
-  a1 = fmaxf(a1, b1);
+  a2 = med3_of(a1, b1, max2_of(a2, b2));
+  a1 = max2_of(a1, b1);
 }
 // Smallest and second smallest of two disjoint sets {a1 <= a2}, {b1 <= b2}.
 __device__ __forceinline__ void min2_merge(int& a1, int& a2, int b1, int b2) {
@@ -278,7 +280,7 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
   }
   const float own1 = a1;
   if (DRAFT) wave_top2(a1, a2);
-  else a1 = wave_reduce(a1, [](float p, float q) { return fmaxf(p, q); });
+  else a1 = wave_reduce(a1, [](float p, float q) { return max2_of(p, q); });
   if (lane == 0) {
     red.top[0][wave] = a1;
     red.top[1][wave] = a2;
@@ -288,7 +290,7 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
   v2 = DRAFT ? red.top[1][0] : kNegInf;
   for (int w = 1; w < kLogitThreads / 64; ++w) {
     if (DRAFT) top2_merge(m, v2, red.top[0][w], red.top[1][w]);
-    else m = fmaxf(m, red.top[0][w]);
+    else m = max2_of(m, red.top[0][w]);
   }
 
   // Entries equal to m are left out of Z''; only waves holding one compare.
@@ -425,7 +427,8 @@ __device__ __forceinline__ float entropy_of(const State& st) { return log1pf(st.
 // ---------------------------------------------------------------------------
 // One (row, chunk) item of the verify rows.
 __device__ __forceinline__ void verify_rows(const VerifyArgs& a, int item, ChunkRed& red) {
-  const int row = item / a.nchunk, c = item % a.nchunk;
+  const int row = item >> a.cshift, c = item & ((1 << a.cshift) - 1);
+  if (c >= a.nchunk) return;  // a slot past the row's last chunk
   const int v0 = c * kLogitChunk, v1 = min(a.vocab, v0 + kLogitChunk);
   float m, v2, z, s;
   int i1, i2;
@@ -436,7 +439,7 @@ __device__ __forceinline__ void verify_rows(const VerifyArgs& a, int item, Chunk
 __global__ __launch_bounds__(kLogitThreads) void verify_rows_kernel(VerifyArgs a) {
   __shared__ ChunkRed red;
   const int item = xcd_item(a.grid_rows);
-  if (item < a.rows * a.nchunk) verify_rows(a, item, red);
+  if (item < (a.rows << a.cshift)) verify_rows(a, item, red);
 }
 
 struct FinalizeLds {
@@ -521,7 +524,8 @@ __global__ __launch_bounds__(kLogitThreads) void verify_finalize_kernel(VerifyAr
 // ---------------------------------------------------------------------------
 // One (row, chunk) item of the draft rows.
 __device__ __forceinline__ void draft_rows(const DraftArgs& a, int item, ChunkRed& red) {
-  const int row = item / a.nchunk, c = item % a.nchunk;
+  const int row = item >> a.cshift, c = item & ((1 << a.cshift) - 1);
+  if (c >= a.nchunk) return;  // a slot past the row's last chunk
   const int v0 = c * kLogitChunk, v1 = min(a.vocab, v0 + kLogitChunk);
   float m, v2, z, s;
   int i1, i2;
@@ -536,7 +540,7 @@ __device__ __forceinline__ void draft_rows(const DraftArgs& a, int item, ChunkRe
 __global__ __launch_bounds__(kLogitThreads) void draft_rows_kernel(DraftArgs a) {
   __shared__ ChunkRed red;
   const int item = xcd_item(a.grid_rows);
-  if (item < a.rows * a.nchunk) draft_rows(a, item, red);
+  if (item < (a.rows << a.cshift)) draft_rows(a, item, red);
 }
 
 // Draft rows blk * (256 / lanes) ...: one lane group per row.
@@ -569,9 +573,9 @@ __global__ __launch_bounds__(kLogitThreads) void draft_finalize_kernel(DraftArgs
 __global__ __launch_bounds__(kLogitThreads) void round_rows_kernel(VerifyArgs v, DraftArgs d, int32_t grid) {
   __shared__ ChunkRed red;
   const int item = xcd_item(grid);
-  const int nv = v.rows * v.nchunk;
+  const int nv = v.rows << v.cshift;
   if (item < nv) verify_rows(v, item, red);
-  else if (item - nv < d.rows * d.nchunk) draft_rows(d, item - nv, red);
+  else if (item - nv < (d.rows << d.cshift)) draft_rows(d, item - nv, red);
 }
 
 __global__ __launch_bounds__(kLogitThreads) void round_finalize_kernel(VerifyArgs v, DraftArgs d) {
@@ -640,7 +644,7 @@ hipError_t launch_draft(const DraftArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_round(const VerifyArgs& v, const DraftArgs& d, hipStream_t stream) {
-  const int64_t items = (int64_t)v.rows * v.nchunk + (int64_t)d.rows * d.nchunk;
+  const int64_t items = ((int64_t)v.rows << v.cshift) + ((int64_t)d.rows << d.cshift);
   const int32_t grid = (int32_t)((items + 7) / 8 * 8);
   if (grid > 0) {
     hipLaunchKernelGGL(round_rows_kernel, dim3(grid), dim3(kLogitThreads), 0, stream, v, d, grid);

@@ -101,6 +101,7 @@ struct VerifyArgs {
   const uint16_t* logits;
   int64_t row_stride;
   int32_t vocab, num_req, rows, nchunk;
+  int32_t cshift;      // row work groups are slots of 2^cshift >= nchunk chunks
   const int32_t* row_indptr;
   const int32_t* tokens;
   int32_t* row_argmax;
@@ -110,13 +111,14 @@ struct VerifyArgs {
   float* accept_entropy;
   float4* chunk_st;    // workspace [rows * nchunk] (max, bits(argmax), Z', S)
   int32_t vec;         // 16-byte loads allowed
-  int32_t grid_rows;   // row work groups (rows * nchunk rounded up to 8)
+  int32_t grid_rows;   // row work groups (rows << cshift rounded up to 8)
 };
 
 struct DraftArgs {
   const uint16_t* logits;
   int64_t row_stride;
   int32_t vocab, rows, nchunk;
+  int32_t cshift;      // as in VerifyArgs
   int32_t* top1;
   int32_t* top2;
   float* p1;
@@ -130,6 +132,13 @@ struct DraftArgs {
 };
 
 inline int32_t logit_chunks(int32_t vocab) { return (vocab + kLogitChunk - 1) / kLogitChunk; }
+// log2 of the chunk slots per row: the smallest power of two >= the row's
+// chunks, so a row work group finds its row and chunk by shift and mask.
+inline int32_t logit_chunk_shift(int32_t vocab) {
+  int32_t s = 0;
+  while ((1 << s) < logit_chunks(vocab)) ++s;
+  return s;
+}
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream);
