@@ -192,11 +192,17 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
   const int M = n * g;
   const int ncg = (M + COLS - 1) / COLS;
   const int nch = (T + p.chunk - 1) / p.chunk;
+  // A request's items run over chunks, then KV heads, then column groups:
+  // the items of one (KV head, chunk) for successive column groups lie
+  // Hkv * chunks apart -- with 8 KV heads, 8 apart, so on the same XCD
+  // (work group b runs on XCD b % 8; every request's items start at a
+  // multiple of 8 then) and dispatched together, and the column groups after
+  // the first mostly find the keys in that XCD's L2 instead of HBM.
   int local = item - rq.item_start;
   const int c = local % nch;
   local /= nch;
-  const int cg = local % ncg;
-  const int hk = local / ncg;
+  const int hk = local % a.hkv;
+  const int cg = local / a.hkv;
   const int kbeg = c * p.chunk;
   const int kend = min(T, kbeg + p.chunk);
 
