@@ -73,7 +73,7 @@
 extern "C" {
 #endif
 
-#define RG_ABI_VERSION 6
+#define RG_ABI_VERSION 7
 
 typedef int32_t rg_status;
 #define RG_OK 0
@@ -82,6 +82,7 @@ typedef int32_t rg_status;
 #define RG_ERR_UNSUPPORTED 3 /* valid but not supported (head_dim, page size) */
 #define RG_ERR_WORKSPACE 4   /* workspace NULL or smaller than required       */
 #define RG_ERR_HIP 5         /* a HIP launch or runtime call failed           */
+#define RG_ERR_WAIT 6        /* a one-launch wait gave up (that call's outputs are invalid) */
 
 /* Version of this ABI (RG_ABI_VERSION of the built library). */
 int32_t rg_abi_version(void);
@@ -151,10 +152,11 @@ rg_status rg_draft_verify_attention_workspace(const rg_attn_layout* layout, size
  * instead as one work-queue launch (the library's variant of mapping mixed
  * ragged attention work onto the compute units, Sec. 5.3): at most one work
  * group per compute unit takes the work items (request, KV head, column
- * group, chunk; costliest request first) and then the merge items from an
- * atomic queue, and a merge item starts as soon as the chunks it merges are
- * done.  It gives the same results within rounding and measured slower on
- * MI355X.  The workspace opens with the queue and per-merge counters, at the
+ * group, chunk; costliest request first) and then the merge items, every one
+ * of them from an atomic queue, and a merge item starts as soon as the
+ * chunks it merges are done (a bounded wait: see
+ * rg_draft_verify_attention_check).  It gives the same results within
+ * rounding and measured slower on MI355X.  The workspace opens with the queue and per-merge counters, at the
  * same place and size for every layout, so one workspace (zeroed once) may
  * serve calls with different layouts one after another.  A launch with more
  * than 16384 merge items always uses the two kernels.
@@ -163,6 +165,21 @@ rg_status rg_draft_verify_attention(const rg_attn_layout* layout, const uint16_t
                                     const uint16_t* k_cache, const uint16_t* v_cache,
                                     uint16_t* out, float* lse, void* ws, size_t ws_bytes,
                                     void* stream);
+
+/*
+ * One-launch mode (RG_ATTN_PERSIST=1) only: whether a merge item's bounded
+ * wait gave up in a call on this attention workspace since the last check.
+ * A correct call never gives up (every chunk a merge item waits for is held
+ * by a running work group); if one did, that call's outputs are not valid.
+ * The kernel moves the flag to a report word in the workspace's
+ * synchronisation words, so it does not carry over into later calls; this
+ * call synchronises `stream`, reads the report word and clears it.
+ *   RG_OK        no wait gave up (or the workspace never ran a one-launch call)
+ *   RG_ERR_WAIT  a wait gave up
+ *   RG_ERR_NULL / RG_ERR_WORKSPACE  ws is NULL / too small to hold the words
+ *   RG_ERR_HIP   the synchronisation or a copy failed
+ */
+rg_status rg_draft_verify_attention_check(void* ws, size_t ws_bytes, void* stream);
 
 /* Planning summary of an attention call (host only, no GPU work): used by
  * tests and tools to inspect how the batch is split. */
@@ -176,8 +193,9 @@ typedef struct rg_attn_plan_info {
   int32_t persistent_launches; /* launches run as one work-queue launch      */
   int32_t sync_words;       /* int32 synchronisation words at sync_offset    */
   int64_t sync_offset;      /* their byte offset in the workspace (-1 without
-                               a workspace); word 2 is nonzero if a merge
-                               item ever gave up waiting (never expected)   */
+                               a workspace); word 3 is nonzero after a call
+                               whose merge item gave up waiting (never
+                               expected; see rg_draft_verify_attention_check) */
 } rg_attn_plan_info;
 rg_status rg_draft_verify_attention_plan(const rg_attn_layout* layout, rg_attn_plan_info* info);
 

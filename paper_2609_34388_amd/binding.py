@@ -24,7 +24,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librecguide
 RG_OK = 0
 NOALLOC_SCRATCH_BYTES = 4 << 20  # RG_NOALLOC_SCRATCH_BYTES
 _STATUS = {0: "ok", 1: "RG_ERR_NULL", 2: "RG_ERR_SHAPE", 3: "RG_ERR_UNSUPPORTED",
-           4: "RG_ERR_WORKSPACE", 5: "RG_ERR_HIP"}
+           4: "RG_ERR_WORKSPACE", 5: "RG_ERR_HIP", 6: "RG_ERR_WAIT"}
 
 
 class RGError(RuntimeError):
@@ -63,7 +63,7 @@ class AttnPlanInfo(ctypes.Structure):
 
 
 EXPORTS = ("rg_abi_version", "rg_status_string", "rg_draft_verify_attention_workspace",
-           "rg_draft_verify_attention", "rg_draft_verify_attention_plan",
+           "rg_draft_verify_attention", "rg_draft_verify_attention_plan", "rg_draft_verify_attention_check",
            "rg_verify_accept_workspace", "rg_verify_accept", "rg_draft_confidence_workspace",
            "rg_draft_confidence", "rg_verify_and_confidence_workspace", "rg_verify_and_confidence",
            "rg_verify_and_confidence_noalloc",
@@ -87,6 +87,7 @@ def _lib():
         "rg_draft_verify_attention_workspace": (I32, [ctypes.POINTER(AttnLayout), ctypes.POINTER(SZ)]),
         "rg_draft_verify_attention_plan": (I32, [ctypes.POINTER(AttnLayout), ctypes.POINTER(AttnPlanInfo)]),
         "rg_draft_verify_attention": (I32, [ctypes.POINTER(AttnLayout), P, P, P, P, P, P, SZ, P]),
+        "rg_draft_verify_attention_check": (I32, [P, SZ, P]),
         "rg_verify_accept_workspace": (I32, [I32, I32, I32, ctypes.POINTER(SZ)]),
         "rg_verify_accept": (I32, [P, I64, I32, I32, I32, P, P, P, P, P, P, P, P, SZ, P]),
         "rg_draft_confidence_workspace": (I32, [I32, I32, ctypes.POINTER(SZ)]),
@@ -242,6 +243,12 @@ def draft_verify_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torc
                                           ws_bytes, _stream(stream))
     _check(st, "rg_draft_verify_attention")
     return out, lse
+
+
+def attention_check(workspace: torch.Tensor, stream=None) -> int:
+    """rg_draft_verify_attention_check: synchronises the stream and returns
+    the status (RG_OK, or 6 = RG_ERR_WAIT when a one-launch wait gave up)."""
+    return int(_lib().rg_draft_verify_attention_check(workspace.data_ptr(), workspace.numel(), _stream(stream)))
 
 
 class _Branches:

@@ -332,6 +332,7 @@ const char* rg_status_string(rg_status s) {
     case RG_ERR_UNSUPPORTED: return "unsupported configuration";
     case RG_ERR_WORKSPACE: return "workspace missing or too small";
     case RG_ERR_HIP: return "HIP launch or runtime error";
+    case RG_ERR_WAIT: return "a one-launch attention wait gave up";
     default: return "unknown status";
   }
 }
@@ -400,6 +401,19 @@ rg_status rg_draft_verify_attention_workspace(const rg_attn_layout* layout, size
   if (st != RG_OK) return st;
   *bytes = fp.ws_bytes;
   return RG_OK;
+}
+
+rg_status rg_draft_verify_attention_check(void* ws, size_t ws_bytes, void* stream) {
+  if (ws == nullptr) return RG_ERR_NULL;
+  if (ws_bytes < (size_t)kSyncHeader * sizeof(int32_t)) return RG_ERR_WORKSPACE;
+  if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess) return RG_ERR_HIP;
+  int32_t* report = static_cast<int32_t*>(ws) + 3;  // sync word 3, at the workspace's start
+  int32_t word = 0;
+  if (hipMemcpy(&word, report, sizeof(word), hipMemcpyDeviceToHost) != hipSuccess) return RG_ERR_HIP;
+  if (word == 0) return RG_OK;
+  const int32_t zero = 0;
+  if (hipMemcpy(report, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return RG_ERR_HIP;
+  return RG_ERR_WAIT;
 }
 
 rg_status rg_draft_verify_attention_plan(const rg_attn_layout* layout, rg_attn_plan_info* info) {

@@ -787,57 +787,59 @@ __global__ __launch_bounds__(kCombRows * PARTS) void attn_combine_kernel(AttnArg
 }
 
 // One-launch work-queue kernel (launches with split requests).  The queue
-// is every main item (costliest request first), then every combine item.  A
-// work group takes its first item by its index (as the dispatcher would) and
-// each further one from an atomic queue head; it asks for the next item at
-// the start of the current one, so the request's latency is hidden.  The
-// combine items of a request run in the same launch, as soon as its chunks
-// are done, on work groups that would otherwise sit idle or exit: no second
-// launch, and no kernel boundary between a split request's chunks and their
-// merge.  The last work group to leave returns the queue head and the exit
-// count to zero for the next call.
+// is every main item (costliest request first), then every combine item.
+// Every work group takes every item, its first included, from an atomic
+// queue head, so an item is only ever held by a work group that is running,
+// and every combine item is taken after every main item: the chunks a
+// combine item waits for are all held by running work groups, and a work
+// group holding a main item as its next one is busy with a main item, which
+// waits for nothing.  A work group asks for its next item at the start of
+// the current one, so the queue's latency is hidden.  The combine items of a
+// request run in the same launch, as soon as its chunks are done, on work
+// groups that would otherwise sit idle or exit: no second launch, and no
+// kernel boundary between a split request's chunks and their merge.  The
+// last work group to leave returns the queue head and the exit count to
+// zero for the next call, and moves a raised give-up flag (sync word 2) to
+// the report word (sync word 3), where rg_draft_verify_attention_check finds
+// it: the flag does not carry over into the next call.
 template <int D, typename Plan>
 __global__ __launch_bounds__(kThreads) void attn_persist_kernel(AttnArgs a, Plan p) {
   constexpr int WORDS = (kKBufs + kVBufs) * kSuper * D / 2;  // 32-bit words of LDS (all of it)
   __shared__ __attribute__((aligned(16))) uint16_t lds[(kKBufs + kVBufs) * kSuper * D];
   // The next item's index passes through the last word of the second V
-  // buffer: no key-group merge area or combine exchange reaches it, and the
-  // next item's first copies (K and V of buffer 0, K of buffer 1) do not
-  // write it before its first barrier.
+  // buffer: no key-group merge area or combine exchange reaches it, and an
+  // item writes that buffer only after its first barrier (buffer 1 goes in
+  // before the second one).
   int* const s_next = reinterpret_cast<int*>(lds) + WORDS - 1;
   static_assert(kCombRowsPersist * kCombPartsPersist == kThreads, "combine items use the whole work group");
   static_assert((kCombPartsPersist - 1) * 10 * kCombRowsPersist < WORDS - 1, "combine exchange below the slot");
   static_assert((kWaves - 1) * (64 * 16 * (D / 32) + 128) < WORDS - 1, "key-group merge area below the slot");
   const int total = p.total_items + p.total_comb;
-  const int grid = p.persist_grid;
-  // First item: the work group's index, which the queue head then continues
-  // from.  When every main item is in this first round, one request's items
-  // are dealt as the main kernel deals them (a head's chunks to one XCD): a
-  // permutation of [0, grid_items), the combine items after it unchanged.
-  int item = (int)blockIdx.x;
-  if (p.num_req == 1 && p.grid_items <= grid && item < p.grid_items) item = xcd_item(p.grid_items);
-  // When every item is in the first round there is no queue: each work group
-  // runs its one item and leaves, with no queue atomics on its way out.
-  const bool queued = total > grid;
+  if (threadIdx.x == 0) *s_next = __hip_atomic_fetch_add(a.sync, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  lds_barrier();
+  int item = *s_next;
   while ((unsigned)item < (unsigned)total) {  // (also stops on a queue head that was not zero)
     int nxt = total;
-    if (queued && threadIdx.x == 0)
-      nxt = grid + __hip_atomic_fetch_add(a.sync, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0) nxt = __hip_atomic_fetch_add(a.sync, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (item < p.total_items)
       attn_item<D, Plan, true>(a, p, item, lds);
     else
       combine_item<D, kCombPartsPersist, kCombRowsPersist, true>(a, p, item - p.total_items,
                                                                 reinterpret_cast<float*>(lds));
-    if (!queued) break;
     lds_barrier();  // every wave is done with LDS
     if (threadIdx.x == 0) *s_next = nxt;
     lds_barrier();
     item = *s_next;
   }
-  if (queued && threadIdx.x == 0 &&
+  if (threadIdx.x == 0 &&
       __hip_atomic_fetch_add(a.sync + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (int)gridDim.x - 1) {
     __hip_atomic_store(a.sync, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(a.sync + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int gave_up = __hip_atomic_load(a.sync + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (gave_up != 0) {
+      __hip_atomic_store(a.sync + 3, gave_up, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a.sync + 2, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 }
 

@@ -13,7 +13,7 @@ constexpr int kPageSize = 16;
 constexpr int kMaxReqPerLaunch = 128;  // equals RG_ATTN_MAX_REQS_PER_LAUNCH
 constexpr int kKeyTile = 128;          // keys per LDS buffer; chunks are multiples of it
 constexpr int kMaxChunkKeys = 1 << 16;  // keys per work item at most
-constexpr int kSyncHeader = 4;          // queue head, exit count, error flag, pad
+constexpr int kSyncHeader = 4;          // queue head, exit count, give-up flag, report word
 // Combine items of one launch the one-launch kernel can count (two counters
 // each); launches with more use the main kernel plus the combine kernel.
 constexpr int kMaxSyncComb = 16384;
@@ -78,9 +78,10 @@ struct AttnArgs {
   const int32_t* page_indices;
   uint16_t* part_o;  // per 32-column tile: 32 x D bf16 normalised partial outputs, MFMA fragment order
   float* part_ml;  // [partial columns][2] fp32 (running max of raw scores, sum)
-  int32_t* sync;   // kSyncWords words, zero between calls: queue head, exit count, error
-                   // flag, pad, then finished-tile counts (indexed by a column group's
-                   // first combine item) and, kMaxSyncComb words on, started-combine counts
+  int32_t* sync;   // kSyncWords words, zero between calls: queue head, exit count, give-up
+                   // flag, report word (nonzero after a call whose wait gave up, until
+                   // read), then finished-tile counts (indexed by a column group's first
+                   // combine item) and, kMaxSyncComb words on, started-combine counts
   int32_t hq, hkv, g;
   float sm_scale;    // natural-log domain scale
   float scale_log2;   // sm_scale * log2(e)

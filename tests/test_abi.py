@@ -37,7 +37,7 @@ def test_abi_version_and_status_strings():
     m = re.search(r"#define RG_ABI_VERSION (\d+)", open(HEADER).read())
     assert binding.abi_version() == int(m.group(1))
     lib = binding.library()
-    for s in range(6):
+    for s in range(7):
         assert lib.rg_status_string(s)
     assert lib.rg_status_string(99) == b"unknown status"
 
@@ -103,6 +103,13 @@ def test_row_counts_past_16_bits_are_rejected():
     st = binding.library().rg_draft_verify_attention_workspace(ctypes.byref(l.c), ctypes.byref(ctypes.c_size_t()))
     assert st == 3
     assert _attn(l) == 3
+
+
+def test_attention_check_validation():
+    lib = binding.library()
+    assert lib.rg_draft_verify_attention_check(None, 1 << 20, None) == 1
+    assert lib.rg_draft_verify_attention_check(ctypes.c_void_p(0x1000), 15, None) == 4
+    assert lib.rg_status_string(6) == b"a one-launch attention wait gave up"
 
 
 def _br(indptr, prefix, lead, rows):

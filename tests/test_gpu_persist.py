@@ -68,6 +68,29 @@ def test_split_parity_both_modes(monkeypatch, persist, case):
     torch.cuda.synchronize()
     check(out, lse, reference(lay, inp))
     assert int(_sync_words(ws, info).abs().sum()) == 0
+    assert binding.attention_check(ws) == 0
+
+
+def test_check_reports_and_clears_the_report_word(monkeypatch):
+    """rg_draft_verify_attention_check reads the report word a one-launch
+    call leaves when a wait gave up (raised here from the host: no wait is
+    made to give up on the device), returns RG_ERR_WAIT once and clears it;
+    the next one-launch call on the workspace runs normally."""
+    monkeypatch.setenv("RG_ATTN_PERSIST", "1")
+    monkeypatch.setenv("RG_ATTN_CHUNK", "128")
+    lay = _custom(2, [700, 300], [8, 4], [8, 4], seed=23)
+    inp = W.make_attention_inputs(lay, DEV, poison=float("nan"))
+    handle = _layout_handle(lay, inp)
+    info = binding.attention_plan(handle)
+    ws = binding.new_workspace(info["workspace_bytes"], DEV)
+    _sync_words(ws, info)[3] = 7
+    assert binding.attention_check(ws) == 6
+    assert int(_sync_words(ws, info)[3]) == 0
+    assert binding.attention_check(ws) == 0
+    out, lse = _run(lay, inp, ws, handle)
+    check(out, lse, reference(lay, inp))
+    assert binding.attention_check(ws) == 0
+    assert int(_sync_words(ws, info).abs().sum()) == 0
 
 
 def test_modes_agree_and_full_size_low(monkeypatch):
