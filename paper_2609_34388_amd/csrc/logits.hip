@@ -38,6 +38,9 @@ constexpr float kLn2 = 0.69314718055994531f;
 constexpr int kU = kLogitChunk / (8 * kLogitThreads);  // 16-byte loads per thread
 constexpr int kE = 8 * kU;                             // entries per thread
 constexpr int kNoIndex = 0x7fffffff;
+// Stands in for an entry set aside: exp(kGone - m) is 0 for any finite m,
+// and so is its product with t; not a bfloat16 value, so no input equals it.
+constexpr float kGone = -1e30f;
 constexpr int kBatchRows = 1024;                       // verify rows scanned per pass
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -147,13 +150,6 @@ __device__ __forceinline__ T wave_reduce(T v, Op op) {
   return op(op(lane_read(v, 0), lane_read(v, 16)), op(lane_read(v, 32), lane_read(v, 48)));
 }
 
-// Largest and second largest value of the multiset {a1 >= a2} U {b1 >= b2}:
-// the runner-up is max(min(a1, b1), max(a2, b2)), which is the median of
-// a1, b1 and max(a2, b2) (that maximum is at most max(a1, b1)).
-__device__ __forceinline__ void top2_merge(float& a1, float& a2, float b1, float b2) {
-  a2 = med3_of(a1, b1, max2_of(a2, b2));
-  a1 = max2_of(a1, b1);
-}
 // Smallest and second smallest of two disjoint sets {a1 <= a2}, {b1 <= b2}.
 __device__ __forceinline__ void min2_merge(int& a1, int& a2, int b1, int b2) {
   a2 = min(max(a1, b1), min(a2, b2));
@@ -161,23 +157,8 @@ __device__ __forceinline__ void min2_merge(int& a1, int& a2, int b1, int b2) {
 }
 
 template <int CTRL>
-__device__ __forceinline__ void top2_step(float& v1, float& v2) {
-  top2_merge(v1, v2, dpp<CTRL>(v1), dpp<CTRL>(v2));
-}
-template <int CTRL>
 __device__ __forceinline__ void min2_step(int& v1, int& v2) {
   min2_merge(v1, v2, dpp<CTRL>(v1), dpp<CTRL>(v2));
-}
-
-__device__ __forceinline__ void wave_top2(float& v1, float& v2) {
-  top2_step<kDppXor1>(v1, v2);
-  top2_step<kDppXor2>(v1, v2);
-  top2_step<kDppHalfMirror>(v1, v2);
-  top2_step<kDppMirror>(v1, v2);
-  float a1 = lane_read(v1, 0), a2 = lane_read(v2, 0);
-  for (int l = 16; l < 64; l += 16) top2_merge(a1, a2, lane_read(v1, l), lane_read(v2, l));
-  v1 = a1;
-  v2 = a2;
 }
 
 __device__ __forceinline__ void wave_min2(int& v1, int& v2) {
@@ -191,15 +172,14 @@ __device__ __forceinline__ void wave_min2(int& v1, int& v2) {
   v2 = a2;
 }
 
-// Z'' and S partial sums of this thread's entries: exp(x - m) over entries
-// below m (all entries when EXCLUDE is false: the caller knows none equals
-// m), and exp(x - m)(x - m) in log2 units.  Entries past the row end are -inf
-// and only occur in a row's last chunk (TAIL), where t is clamped so that
-// e * t stays 0.  Two independent accumulator chains halve the dependent
-// latency.
-template <bool TAIL, bool EXCLUDE>
-__device__ __forceinline__ void exp_sums(const float (&x)[kE], float m, float& zz, float& ss) {
-  const float mc = m * kLog2e;
+// Z'' and S partial sums of this thread's entries against the chunk maximum
+// m (mc = m log2 e): exp(x - m) and exp(x - m)(x - m) in log2 units, in two
+// independent chains to halve the dependent latency.  Entries equal to m
+// have been replaced by kGone, whose terms are exactly 0.  Entries past the
+// row end are -inf and only occur in a row's last chunk (TAIL), where t is
+// clamped so that e * t stays 0.
+template <bool TAIL>
+__device__ __forceinline__ void exp_sums(const float (&x)[kE], float mc, float& zz, float& ss) {
   float z0 = 0.f, z1 = 0.f, s0 = 0.f, s1 = 0.f;
 #pragma unroll
   for (int k = 0; k < kE; k += 2) {
@@ -209,12 +189,8 @@ __device__ __forceinline__ void exp_sums(const float (&x)[kE], float m, float& z
       t0 = fmaxf(t0, -1000.f);
       t1 = fmaxf(t1, -1000.f);
     }
-    float e0 = __builtin_amdgcn_exp2f(t0);
-    float e1 = __builtin_amdgcn_exp2f(t1);
-    if (EXCLUDE) {
-      e0 = (x[k] == m) ? 0.f : e0;
-      e1 = (x[k + 1] == m) ? 0.f : e1;
-    }
+    const float e0 = __builtin_amdgcn_exp2f(t0);
+    const float e1 = __builtin_amdgcn_exp2f(t1);
     z0 += e0;
     z1 += e1;
     s0 = __builtin_fmaf(e0, t0, s0);
@@ -225,19 +201,55 @@ __device__ __forceinline__ void exp_sums(const float (&x)[kE], float m, float& z
 }
 
 struct ChunkRed {
-  float top[2][4];  // per wave: largest, second largest value
-  float zs[2][4];   // per wave: Z'' and S partial sums
-  int cnt[4];       // per wave: entries equal to the chunk maximum
-  int idx[3][4];    // per wave: first, second index of the maximum; first index of the runner-up
+  float m[4];      // per wave: largest value
+  float zs[2][4];  // per wave: Z'' and S partial sums
+  float c2[4];     // per wave: largest value once one entry holding m is set aside
+  int cnt[4];      // per wave: entries equal to the chunk maximum
+  int f[2][4];     // per wave: first, second index of the maximum
+  int g[4];        // per wave: first index of the runner-up
 };
 
-// One chunk of one row -> (m, i1, v2, i2, Z', S) in two reduction rounds.
-// Round 1: the chunk maximum m (and, for draft rows, the runner-up value v2,
-// equal to m when the maximum occurs twice).  Round 2, in one pass over the
-// registers: Z'' = sum of exp(x - m) over entries below m, S, the number of
-// entries equal to m, the two lowest indices holding m and the lowest index
-// holding v2.  Then Z' (all but the top entry) = Z'' + (count - 1), exactly.
-// Only thread 0 receives (i1, i2, Z', S).
+// Sets aside this thread's entries equal to the chunk maximum m: counts
+// them, keeps their two lowest indices and replaces them by kGone.  Only
+// groups where some lane holds m are visited (usually one group of one lane
+// per chunk; the test is wave-uniform), in descending order so that the
+// lowest index is assigned last.  For draft rows a group's maximum that
+// equals m becomes the group's second largest value (m again if m occurs
+// twice in it), so that the largest of the thread's group maxima is its
+// runner-up whenever the chunk holds m once.
+template <bool DRAFT>
+__device__ __forceinline__ void set_aside_max(float (&x)[kE], float (&gm)[kU], float m, int v0, int& cnt,
+                                              int& f1, int& f2, bool& hit) {
+#pragma unroll
+  for (int u = kU - 1; u >= 0; --u) {
+    if (__any(gm[u] == m)) {
+      hit = true;
+      float* y = x + 8 * u;
+      float t1 = kNegInf, t2 = kNegInf;  // t1 >= t2: the group's two largest values
+#pragma unroll
+      for (int j = 7; j >= 0; --j) {
+        if (DRAFT) {
+          t2 = med3_of(t1, t2, y[j]);
+          t1 = max2_of(t1, y[j]);
+        }
+        const bool eq = y[j] == m;  // selects, not branches: no copies where groups join
+        cnt += eq ? 1 : 0;
+        f2 = eq ? f1 : f2;
+        f1 = eq ? entry_index(v0, 8 * u + j) : f1;
+        y[j] = eq ? kGone : y[j];
+      }
+      if (DRAFT && gm[u] == m) gm[u] = t2;
+    }
+  }
+}
+
+// One chunk of one row -> (m, i1, v2, i2, Z', S).  Round 1: the chunk
+// maximum m.  Round 2: Z'' = sum of exp(x - m) over entries below m, S, the
+// number of entries equal to m and their two lowest indices; for draft rows
+// also the runner-up v2 (m again when m occurs twice, else the largest value
+// below m).  Round 3 (draft rows with m once): the lowest index holding v2.
+// Then Z' (all but the top entry) = Z'' + (count - 1), exactly.  Only thread
+// 0 receives (i1, i2, Z', S).
 template <bool DRAFT>
 __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1, bool vec, ChunkRed& red,
                                             float& m, int& i1, float& v2, int& i2, float& z, float& s) {
@@ -246,123 +258,87 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
   load_chunk(row, v0, v1, vec, x);
 
   // Maximum of each group of 8 entries (one 16-byte load: consecutive
-  // vocabulary indices) and this thread's largest entry; for draft rows also
-  // each group's and the thread's runner-up.  Groups are independent chains;
-  // with t1 >= t2, the runner-up after adding x is the median of (t1, t2, x).
+  // vocabulary indices) and of this thread's entries.
   float gm[kU];
-  float a1, a2 = kNegInf;
-  if (DRAFT) {
-    float g2[kU];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      float t1 = kNegInf, t2 = kNegInf;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        t2 = med3_of(t1, t2, x[8 * u + j]);
-        t1 = max2_of(t1, x[8 * u + j]);
-      }
-      gm[u] = t1;
-      g2[u] = t2;
-    }
-    a1 = gm[0];
-    a2 = g2[0];
-#pragma unroll
-    for (int u = 1; u < kU; ++u) top2_merge(a1, a2, gm[u], g2[u]);
-  } else {
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const float* y = x + 8 * u;
-      gm[u] = max3_of(max3_of(y[0], y[1], y[2]), max3_of(y[3], y[4], y[5]), max2_of(y[6], y[7]));
-    }
-    a1 = gm[0];
-#pragma unroll
-    for (int u = 1; u < kU; ++u) a1 = max2_of(a1, gm[u]);
+  for (int u = 0; u < kU; ++u) {
+    const float* y = x + 8 * u;
+    gm[u] = max3_of(max3_of(y[0], y[1], y[2]), max3_of(y[3], y[4], y[5]), max2_of(y[6], y[7]));
   }
-  const float own1 = a1;
-  if (DRAFT) wave_top2(a1, a2);
-  else a1 = wave_reduce(a1, [](float p, float q) { return max2_of(p, q); });
-  if (lane == 0) {
-    red.top[0][wave] = a1;
-    red.top[1][wave] = a2;
-  }
+  float a1 = gm[0];
+#pragma unroll
+  for (int u = 1; u < kU; ++u) a1 = max2_of(a1, gm[u]);
+  const auto fmax2 = [](float p, float q) { return max2_of(p, q); };
+  a1 = wave_reduce(a1, fmax2);
+  if (lane == 0) red.m[wave] = a1;
   __syncthreads();
-  m = red.top[0][0];
-  v2 = DRAFT ? red.top[1][0] : kNegInf;
-  for (int w = 1; w < kLogitThreads / 64; ++w) {
-    if (DRAFT) top2_merge(m, v2, red.top[0][w], red.top[1][w]);
-    else m = max2_of(m, red.top[0][w]);
-  }
+  m = max2_of(max2_of(red.m[0], red.m[1]), max2_of(red.m[2], red.m[3]));
 
-  // Entries equal to m are left out of Z''; only waves holding one compare.
-  float zz, ss;
-  const bool exclude = __any(own1 == m);
-  if (v0 + kLogitChunk <= v1) {
-    if (exclude) exp_sums<false, true>(x, m, zz, ss);
-    else exp_sums<false, false>(x, m, zz, ss);
-  } else {
-    if (exclude) exp_sums<true, true>(x, m, zz, ss);
-    else exp_sums<true, false>(x, m, zz, ss);
-  }
-  // Count and indices of the maximum (and, for draft rows, the first index of
-  // the runner-up value): only groups whose maximum reaches m (or v2) can hold
-  // them -- usually one group of one lane per chunk -- so only those groups
-  // are scanned, and only waves that scanned reduce the results.
-  const bool has_v2 = DRAFT && v2 != kNegInf;
-  const float thr = has_v2 ? v2 : m;  // v2 <= m
-  int cnt = 0, f1 = kNoIndex, f2 = kNoIndex, g = kNoIndex;
-  bool scanned = false;
+  int cnt = 0, f1 = kNoIndex, f2 = kNoIndex;
+  bool hit = false;
+  set_aside_max<DRAFT>(x, gm, m, v0, cnt, f1, f2, hit);
+  float zz, ss, c2 = kNegInf;
+  if (v0 + kLogitChunk <= v1) exp_sums<false>(x, m * kLog2e, zz, ss);
+  else exp_sums<true>(x, m * kLog2e, zz, ss);
+  if (DRAFT) {
+    c2 = gm[0];
 #pragma unroll
-  for (int u = kU - 1; u >= 0; --u) {  // descending, so the lowest index is assigned last
-    if (gm[u] >= thr) {
-      scanned = true;
-#pragma unroll
-      for (int j = 7; j >= 0; --j) {
-        const int idx = entry_index(v0, 8 * u + j);
-        if (x[8 * u + j] == m) {
-          ++cnt;
-          f2 = f1;
-          f1 = idx;
-        }
-        if (has_v2 && x[8 * u + j] == v2) g = idx;
-      }
-    }
+    for (int u = 1; u < kU; ++u) c2 = max2_of(c2, gm[u]);
   }
   const auto add = [](float p, float q) { return p + q; };
+  const auto imin = [](int p, int q) { return min(p, q); };
   zz = wave_reduce(zz, add);
   ss = wave_reduce(ss, add);
-  if (__any(scanned)) {
+  if (DRAFT) c2 = wave_reduce(c2, fmax2);
+  if (hit) {  // wave-uniform
     cnt = wave_reduce(cnt, [](int p, int q) { return p + q; });
-    const auto imin = [](int p, int q) { return min(p, q); };
-    if (DRAFT) {
-      wave_min2(f1, f2);
-      g = wave_reduce(g, imin);
-    } else {
-      f1 = wave_reduce(f1, imin);
-    }
+    if (DRAFT) wave_min2(f1, f2);
+    else f1 = wave_reduce(f1, imin);
   }
   if (lane == 0) {
     red.zs[0][wave] = zz;
     red.zs[1][wave] = ss;
+    red.c2[wave] = c2;
     red.cnt[wave] = cnt;
-    red.idx[0][wave] = f1;
-    red.idx[1][wave] = f2;
-    red.idx[2][wave] = g;
+    red.f[0][wave] = f1;
+    red.f[1][wave] = f2;
   }
   __syncthreads();
+  int g = kNoIndex;
+  v2 = kNegInf;
+  if (DRAFT) {
+    cnt = (red.cnt[0] + red.cnt[1]) + (red.cnt[2] + red.cnt[3]);
+    v2 = cnt >= 2 ? m : max2_of(max2_of(red.c2[0], red.c2[1]), max2_of(red.c2[2], red.c2[3]));
+    if (cnt < 2 && v2 != kNegInf) {  // block-uniform
+      // Only groups whose maximum reaches v2 can hold it.
+      bool scanned = false;
+#pragma unroll
+      for (int u = kU - 1; u >= 0; --u) {
+        if (__any(gm[u] >= v2)) {
+          scanned = true;
+#pragma unroll
+          for (int j = 7; j >= 0; --j)
+            if (x[8 * u + j] == v2) g = entry_index(v0, 8 * u + j);
+        }
+      }
+      if (scanned) g = wave_reduce(g, imin);
+      if (lane == 0) red.g[wave] = g;
+      __syncthreads();
+      g = min(min(red.g[0], red.g[1]), min(red.g[2], red.g[3]));
+    }
+  }
   if (threadIdx.x != 0) return;
   zz = (red.zs[0][0] + red.zs[0][1]) + (red.zs[0][2] + red.zs[0][3]);
   ss = (red.zs[1][0] + red.zs[1][1]) + (red.zs[1][2] + red.zs[1][3]);
-  cnt = red.cnt[0] + red.cnt[1] + red.cnt[2] + red.cnt[3];
-  f1 = red.idx[0][0];
-  f2 = red.idx[1][0];
-  g = red.idx[2][0];
+  cnt = (red.cnt[0] + red.cnt[1]) + (red.cnt[2] + red.cnt[3]);
+  f1 = red.f[0][0];
+  f2 = red.f[1][0];
   for (int w = 1; w < kLogitThreads / 64; ++w) {
-    if (DRAFT) min2_merge(f1, f2, red.idx[0][w], red.idx[1][w]);
-    else f1 = min(f1, red.idx[0][w]);
-    g = min(g, red.idx[2][w]);
+    if (DRAFT) min2_merge(f1, f2, red.f[0][w], red.f[1][w]);
+    else f1 = min(f1, red.f[0][w]);
   }
   i1 = f1;
-  i2 = !DRAFT ? kNoIndex : (v2 == m ? f2 : g);
+  i2 = !DRAFT ? kNoIndex : (cnt >= 2 ? f2 : g);
   z = zz + (float)(cnt - 1);
   s = ss * kLn2;
 }

@@ -89,7 +89,7 @@ def test_peaked_rows_entropy_accuracy():
     check_draft(logits, run_draft(logits))
 
 
-@pytest.mark.parametrize("vocab", [2, 7, 1000, 8192, 8193, 128250])
+@pytest.mark.parametrize("vocab", [2, 7, 1000, 8192, 8193, 16384, 16385, 128250])
 def test_vocab_sizes_and_tails(vocab):
     g = torch.Generator(device=DEV).manual_seed(vocab)
     logits = (torch.randn(9, vocab, generator=g, device=DEV) * 2).to(torch.bfloat16)

@@ -40,9 +40,9 @@ def test_noalloc_round_matches_workspace_round(first, second):
 def test_noalloc_round_refuses_batches_past_the_scratch():
     lib = binding.library()
     n = ctypes.c_size_t()
-    assert lib.rg_verify_and_confidence_workspace(1, 8000, 8000, 128256, ctypes.byref(n)) == 0
+    assert lib.rg_verify_and_confidence_workspace(1, 16000, 16000, 128256, ctypes.byref(n)) == 0
     assert n.value > binding.NOALLOC_SCRATCH_BYTES
     D = ctypes.c_void_p(0x1000)  # never dereferenced: the size check comes first
-    st = lib.rg_verify_and_confidence_noalloc(D, 128256, D, 128256, 128256, 1, 8000, D, D, D, D, D, None, None,
-                                              8000, D, D, D, D, None, None, None)
+    st = lib.rg_verify_and_confidence_noalloc(D, 128256, D, 128256, 128256, 1, 16000, D, D, D, D, D, None, None,
+                                              16000, D, D, D, D, None, None, None)
     assert st == 3
