@@ -156,7 +156,7 @@ def overlap_work(ov, branches):
     return nbytes, 4 * D * hq * pairs
 
 
-def overlap_leg(lay, dev, steps, warmup, capture, timed, step_outputs):
+def overlap_leg(lay, dev, steps, warmup, capture, timed, step_outputs, quadratic=True):
     """Sec. 5.1 / 5.3 measured on the step's workload: every request's rows
     after its verify rows become overlap branches (two corrections and a
     continuation, each with the request's draft block size), served by one
@@ -240,6 +240,22 @@ def overlap_leg(lay, dev, steps, warmup, capture, timed, step_outputs):
     ov_bytes, ov_flops = overlap_work(ov, branches)
     sep_bytes = algorithmic_work(sep)["attn_bytes"]
     del sets, base, kb, vb
+    result = {
+        "branches": len(flat), "requests": lay.num_requests, "rows": ov.total_q,
+        "kv_tokens": int(ov.kv_len.sum()), "input_copies_rotated": copies,
+        "multibranch": {"us": round(mb_ms * 1e3, 3), "bytes": ov_bytes, "flops": ov_flops,
+                        "gbps": round(ov_bytes / (mb_ms * 1e-3) / 1e9, 1),
+                        "frac_hbm": round(ov_bytes / (mb_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                        "tflops": round(ov_flops / (mb_ms * 1e-3) / 1e12, 3)},
+        "separate_requests": {"us": round(sep_ms * 1e3, 3), "requests": sep.num_requests,
+                              "bytes": sep_bytes, "gbps": round(sep_bytes / (sep_ms * 1e-3) / 1e9, 1)},
+        "speedup_vs_separate": round(sep_ms / mb_ms, 3),
+        "bytes_saved": sep_bytes - ov_bytes,
+        "max_row_diff_vs_separate": float(f"{row_err:.3e}"),
+        "plan_branches_us": round(plan_ms * 1e3, 3), "match_branches_us": round(match_ms * 1e3, 3),
+    }
+    if not quadratic:
+        return result
 
     # The quadratic layout of Sec. 6.2 on the same requests: one draft block
     # per hypothetical accepted length, through the same entry point.
@@ -265,25 +281,12 @@ def overlap_leg(lay, dev, steps, warmup, capture, timed, step_outputs):
     q_ms = timed(quadratic)
     q_bytes, q_flops = overlap_work(qov, qbr)
     del qin, qsets
-    return {
-        "branches": len(flat), "requests": lay.num_requests, "rows": ov.total_q,
-        "kv_tokens": int(ov.kv_len.sum()), "input_copies_rotated": copies,
-        "multibranch": {"us": round(mb_ms * 1e3, 3), "bytes": ov_bytes, "flops": ov_flops,
-                        "gbps": round(ov_bytes / (mb_ms * 1e-3) / 1e9, 1),
-                        "frac_hbm": round(ov_bytes / (mb_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
-                        "tflops": round(ov_flops / (mb_ms * 1e-3) / 1e12, 3)},
-        "separate_requests": {"us": round(sep_ms * 1e3, 3), "requests": sep.num_requests,
-                              "bytes": sep_bytes, "gbps": round(sep_bytes / (sep_ms * 1e-3) / 1e9, 1)},
-        "speedup_vs_separate": round(sep_ms / mb_ms, 3),
-        "bytes_saved": sep_bytes - ov_bytes,
-        "max_row_diff_vs_separate": float(f"{row_err:.3e}"),
-        "plan_branches_us": round(plan_ms * 1e3, 3), "match_branches_us": round(match_ms * 1e3, 3),
-        "quadratic_layout": {"branches": len(qflat), "rows": qov.total_q, "input_copies_rotated": qcopies, "us": round(q_ms * 1e3, 3),
-                             "bytes": q_bytes, "flops": q_flops,
-                             "gbps": round(q_bytes / (q_ms * 1e-3) / 1e9, 1),
-                             "tflops": round(q_flops / (q_ms * 1e-3) / 1e12, 3),
-                             "time_vs_three_branches": round(q_ms / mb_ms, 3)},
-    }
+    result["quadratic_layout"] = {"branches": len(qflat), "rows": qov.total_q, "input_copies_rotated": qcopies,
+                                  "us": round(q_ms * 1e3, 3), "bytes": q_bytes, "flops": q_flops,
+                                  "gbps": round(q_bytes / (q_ms * 1e-3) / 1e9, 1),
+                                  "tflops": round(q_flops / (q_ms * 1e-3) / 1e12, 3),
+                                  "time_vs_three_branches": round(q_ms / mb_ms, 3)}
+    return result
 
 
 def _gather(L, inputs, reqs):
@@ -705,6 +708,8 @@ def main(argv=None):
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overlap", action="store_true", help="skip the overlap-round measurement")
+    ap.add_argument("--no-quadratic", action="store_true",
+                    help="in the overlap-round measurement, skip the quadratic layout")
     ap.add_argument("--no-block-sizing", action="store_true", help="skip the block-sizing measurement")
     ap.add_argument("--no-all-configs", action="store_true",
                     help="skip the per-workload summary of the other configurations")
@@ -789,7 +794,8 @@ def main(argv=None):
             result[k] = m[k]
     if not args.no_overlap:
         result["overlap"] = overlap_leg(lay, dev, args.steps, args.warmup, m["capture"], m["time_calls"],
-                                        (m["vout"], m["dout"], torch.as_tensor(lay.draft_row_indptr, device=dev)))
+                                        (m["vout"], m["dout"], torch.as_tensor(lay.draft_row_indptr, device=dev)),
+                                        quadratic=not args.no_quadratic)
     if not args.no_block_sizing:
         result["block_sizing"] = block_sizing_leg(lay, dev, m["time_calls"])
     if not args.no_cpu_baseline:

@@ -2,8 +2,8 @@
 under profiles/ (kernel trace, HBM traffic with the copy calibration and the
 record bench.py reads, compute-side counters).
 
-Usage: python -m paper_2609_34388_amd.profile_summary <out-dir> <workload> [...]
-(<out-dir> as given to profile_runs.sh; writes profiles/<kind>_<workload>*.md).
+Usage: python -m paper_2609_34388_amd.profile_summary <out-dir> <workload | overlap:workload> [...]
+(<out-dir> and entries as given to profile_runs.sh; writes profiles/*_<workload>*.md).
 """
 from __future__ import annotations
 
@@ -21,7 +21,8 @@ sys.path.insert(0, ROOT)
 import bench  # noqa: E402
 
 RUNS = "bash paper_2609_34388_amd/profile_runs.sh <out-dir> {wl}"
-BENCH = "python3 bench.py --no-overlap --no-block-sizing --no-cpu-baseline --no-all-configs --workload {wl}"
+BENCH = "python3 bench.py --no-block-sizing --no-cpu-baseline --no-all-configs --no-overlap --workload {wl}"
+BENCH_OV = "python3 bench.py --no-block-sizing --no-cpu-baseline --no-all-configs --no-quadratic --workload {wl}"
 
 
 def short(name: str) -> str:
@@ -172,9 +173,67 @@ def sq_md(out: str, wl: str) -> str:
     return "\n".join(lines)
 
 
+def overlap_md(out: str, wl: str) -> str:
+    tag = f"overlap_{wl}"
+    rows = list(csv.DictReader(open(one(f"{out}/trace_{tag}/*kernel_stats.csv"))))
+    b = bench_line(f"{out}/trace_{tag}.log")
+    ov = b["overlap"]
+    cal = calibration(out)
+    ff, wf = cal["FETCH_SIZE"][2], cal["WRITE_SIZE"][2]
+    fetch = per_kernel(counter_rows(one(f"{out}/pmc_FETCH_SIZE_{tag}/*counter_collection.csv")), "FETCH_SIZE")
+    write = per_kernel(counter_rows(one(f"{out}/pmc_WRITE_SIZE_{tag}/*counter_collection.csv")), "WRITE_SIZE")
+    launches = (ov["requests"] + 63) // 64  # the branched plan holds 64 requests per launch
+    lines = [f"# Multi-branch attention of the overlap round, workload `{wl}`: kernel trace and HBM traffic", "",
+             f"The overlap round of the benchmark on `{wl}` ({ov['requests']} requests, {ov['branches']} branches, "
+             f"{ov['rows']} query rows, {ov['kv_tokens']} keys): every request keeps its verify rows and gets two "
+             "correction branches (a committed replacement token plus a draft block of the request's block size) "
+             "and a continuation branch, served by one rg_multibranch_attention call that reads each request's "
+             "keys once; the comparison serves the same rows and keys as separate requests through "
+             "rg_draft_verify_attention.", "",
+             "Commands (repository root on the GPU host; the overlap entry of):", "", "```",
+             f"bash paper_2609_34388_amd/profile_runs.sh <out-dir> overlap:{wl}",
+             f"# i.e. rocprofv3 --kernel-trace --stats --output-format csv -d <out-dir>/trace_{tag} -o {tag} -- "
+             + BENCH_OV.format(wl=wl) + " --steps 20 --warmup 5",
+             f"#   and for c in FETCH_SIZE WRITE_SIZE: rocprofv3 --pmc $c --output-format csv -d "
+             f"<out-dir>/pmc_${{c}}_{tag} -o {tag} -- " + BENCH_OV.format(wl=wl) + " --steps 3 --warmup 1",
+             "```", "", "| kernel | calls | mean us |", "|---|---|---|"]
+    for r in rows:
+        n = short(r["Name"])
+        if "AttnReqBr" in n or "branches_kernel" in n:
+            lines.append(f"| {n} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} |")
+    by = 0.0
+    fk = wk = 0.0
+    for k in fetch:
+        if "AttnReqBr" in k:
+            f_, w_ = statistics.mean(fetch[k]), statistics.mean(write.get(k, [0.0]))
+            fk += f_
+            wk += w_
+            by += (f_ * ff + w_ * wf) * 1024
+    by *= launches  # every branched kernel runs once per launch
+    fk *= launches
+    wk *= launches
+    alg = ov["multibranch"]["bytes"]
+    lines += ["", f"rg_multibranch_attention = {launches} launch(es) per call (at most 64 requests per launch).", "",
+              "| per call | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM MB (scaled) | algorithmic MB | ratio |",
+              "|---|---|---|---|---|---|",
+              f"| rg_multibranch_attention | {fk:.0f} | {wk:.0f} | {by / 1e6:.1f} | {alg / 1e6:.1f} | {by / alg:.3f} |",
+              "", f"Counter scaling from the plain-copy calibration of the same run: FETCH_SIZE x {ff:.4f}, "
+              f"WRITE_SIZE x {wf:.4f}.", "", "Bench (graph replay, profiler attached):", "", "```",
+              json.dumps(ov), "```", ""]
+    return "\n".join(lines)
+
+
 def main(argv):
-    out, wls = argv[0], argv[1:]
-    for wl in wls:
+    out, entries = argv[0], argv[1:]
+    for e in entries:
+        if e.startswith("overlap:"):
+            wl = e.split(":", 1)[1]
+            path = os.path.join(ROOT, "profiles", f"multibranch_{wl}_trace_and_traffic.md")
+            with open(path, "w") as f:
+                f.write(overlap_md(out, wl))
+            print("wrote", path)
+            continue
+        wl = e
         for name, fn in ((f"step_{wl}_kernel_trace.md", trace_md), (f"attention_{wl}_traffic.md", traffic_md),
                          (f"compute_counters_{wl}.md", sq_md)):
             path = os.path.join(ROOT, "profiles", name)
