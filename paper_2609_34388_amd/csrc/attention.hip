@@ -248,10 +248,22 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
   const int pw = wave - kWaves;
   const int par = pw / WPG;  // wave-uniform: buffer parity (and LDS slot) of this copy wave
   const int q = pw % WPG;
+  // A buffer's 8 page numbers: one 32-byte scalar load when all 8 are the
+  // chunk's (else one load per slot, repeating the last page), so the copies
+  // wait for one scalar round trip, not eight.
+  typedef int32_t i32x8 __attribute__((ext_vector_type(8), aligned(4)));
+  typedef const i32x8 __attribute__((address_space(4))) * cpage8_ptr;
+  static_assert(kSuper / kPageSize == 8, "eight pages per buffer");
   auto read_pages = [&](int s, int (&pg)[kSuper / kPageSize]) {
     const int base = s * (kSuper / kPageSize);
+    if (base + 8 <= npg) {
+      const i32x8 v = *(cpage8_ptr)(chunk_pages + base);
 #pragma unroll
-    for (int j = 0; j < kSuper / kPageSize; ++j) pg[j] = chunk_pages[min(base + j, npg - 1)];
+      for (int j = 0; j < 8; ++j) pg[j] = v[j];
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pg[j] = chunk_pages[min(base + j, npg - 1)];
+    }
   };
   // A lane's byte offset inside its page repeats with period 2 in i: blocks
   // i and i + 2 lie 2 WPG = 4 blocks apart, 4 KPB keys (a multiple of 16,
@@ -316,12 +328,14 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
     // start) and land in LDS slot s % 2 before barrier s -- over buffer
     // s - 2, computed before barrier s - 1 -- so two buffers are in flight
     // per work group, one per pair, and each wave waits only for its own.
-    // The page numbers come from the scalar cache just before the loads.
+    // A pair reads the page numbers of its next buffer right after issuing
+    // the loads of the current one, so they are in registers when needed.
     u32x4 r[2 * NB];
     int pg[kSuper / kPageSize];
     if (par < nsup) {
       read_pages(par, pg);
       load_set(pg, r);
+      if (par + 2 < nsup) read_pages(par + 2, pg);
     }
     for (int s = 0; s < nsup; ++s) {
       const bool mine = (s & 1) == par;
@@ -330,8 +344,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
       const int nvalid = kend - (kbeg + s * kSuper);
       if (nvalid < kSuper) tail_fixup(s, nvalid);
       if (mine && s + 2 < nsup) {
-        read_pages(s + 2, pg);
-        load_set(pg, r);
+        load_set(pg, r);  // buffer s + 2, whose page numbers were fetched a round earlier
+        if (s + 4 < nsup) read_pages(s + 4, pg);
       }
     }
     if constexpr (PERSIST) {
