@@ -233,7 +233,9 @@ rg_status plan_attention(const rg_attn_layout* L, const rg_branch_layout* B, Ful
   for (int r = 0; r < R; ++r) {
     const int64_t n = L->q_indptr[r + 1] - L->q_indptr[r];
     const int64_t T = (int64_t)L->ctx_len[r] + n;
-    const int64_t tiles = std::min<int64_t>(8, (n * g + 31) / 32);
+    const int64_t all_tiles = (n * g + 31) / 32;
+    const int64_t groups = std::max<int64_t>(1, (all_tiles + 7) / 8);
+    const int64_t tiles = (all_tiles + groups - 1) / groups;  // the widest column group's (tiles dealt evenly)
     const int64_t bufs = (std::min<int64_t>(T, fp.chunk) + kKeyTile - 1) / kKeyTile;
     cost[r] = n == 0 ? 0.0 : 2.0 + (double)bufs * std::max(1.0, (double)tiles / 4.0);
   }

@@ -191,6 +191,10 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
   const int g = a.g;
   const int M = n * g;
   const int ncg = (M + COLS - 1) / COLS;
+  // The request's 32-column tiles are dealt evenly to its column groups
+  // (e.g. 17 tiles as 6, 6, 5 rather than 8, 8, 1), so the groups, which
+  // read the same keys, run at about the same pace.
+  const int tpg = ((M + 31) / 32 + ncg - 1) / ncg;
   const int nch = (T + p.chunk - 1) / p.chunk;
   // A request's items run over chunks, then KV heads, then column groups:
   // the items of one (KV head, chunk) for successive column groups lie
@@ -216,7 +220,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
   // 8 / nct' waves (nct' = nct rounded up to a power of two).  5 to 7 tiles:
   // tiles 0-3 get waves 0-3 and the rest share waves 4-7 by key groups, so
   // no SIMD carries two whole tiles while another idles.
-  const int nct = min(kWaves, (M - cg * COLS + 31) / 32);
+  const int nct = min(tpg, (M + 31) / 32 - cg * tpg);
   const bool producer = wave >= kWaves;  // wave-uniform: copy wave
   // Pages of this chunk: entries pg0 .. pg0 + npg - 1 of the request's list.
   const int pg0 = kbeg / kPageSize;
@@ -380,7 +384,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
     kstride = 1;
   }
   const bool tile_on = !producer && ct < nct;  // wave-uniform
-  const int col = cg * COLS + ct * 32 + lc;
+  const int col = (cg * tpg + ct) * 32 + lc;
   const bool valid = tile_on && col < M;
   const int tok = valid ? col / g : 0;
   const int hh = col - tok * g;
@@ -600,7 +604,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, const Plan& p, cons
     // the point every XCD reads from before the wave's wait below ends), and
     // then the wave adds its tile to the column group's finished count.
     const int M32 = (M + 31) & ~31;
-    const size_t tile0 = (size_t)rq.part_start + ((size_t)hk * nch + c) * M32 + (size_t)(cg * COLS + ct * 32);
+    const size_t tile0 = (size_t)rq.part_start + ((size_t)hk * nch + c) * M32 + (size_t)((cg * tpg + ct) * 32);
     uint16_t* dst = a.part_o + tile0 * D;
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;  // 0: no key of this chunk is visible to the column
     if (valid) {
@@ -671,9 +675,10 @@ __device__ __forceinline__ void combine_item(const AttnArgs& a, const Plan& p, c
   const size_t base = (size_t)rq.part_start + (size_t)hk * nch * M32 + (size_t)tile * 32;
 
   if constexpr (PERSIST) {
-    constexpr int TPG = 256 / 32;  // tiles per column group
-    const int cg = tile / TPG, ncg = (M + 255) / 256;
-    const int nct = min(TPG, tiles - cg * TPG);
+    const int ncg = (M + 255) / 256;
+    const int tpg = (tiles + ncg - 1) / ncg;  // tiles per column group, as the main items deal them
+    const int cg = tile / tpg;
+    const int nct = min(tpg, tiles - cg * tpg);
     int32_t* done = a.sync + kSyncHeader + rq.comb_start + hk * ncg + cg;
     if (threadIdx.x == 0) {
       const int target = nch * nct;
