@@ -61,7 +61,9 @@
  *   to zero), so zeroing it once when it is allocated is enough.  The other
  *   workspaces need no initialisation.  Contents are otherwise meaningless
  *   after a call.  Two calls in flight at once must not share a workspace.
- * - Inputs must be finite.
+ * - Inputs must be finite, and logits of magnitude below 2^127 (about
+ *   1.7e38): the vocabulary passes scale logits by log2(e), which must not
+ *   overflow.  A masked vocabulary entry can hold e.g. -1e30.
  */
 #ifndef RECGUIDE_H
 #define RECGUIDE_H

@@ -38,9 +38,6 @@ constexpr float kLn2 = 0.69314718055994531f;
 constexpr int kU = kLogitChunk / (8 * kLogitThreads);  // 16-byte loads per thread
 constexpr int kE = 8 * kU;                             // entries per thread
 constexpr int kNoIndex = 0x7fffffff;
-// Stands in for an entry set aside: exp(kGone - m) is 0 for any finite m,
-// and so is its product with t; not a bfloat16 value, so no input equals it.
-constexpr float kGone = -1e30f;
 constexpr int kBatchRows = 1024;                       // verify rows scanned per pass
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -175,7 +172,7 @@ __device__ __forceinline__ void wave_min2(int& v1, int& v2) {
 // Z'' and S partial sums of this thread's entries against the chunk maximum
 // m (mc = m log2 e): exp(x - m) and exp(x - m)(x - m) in log2 units, in two
 // independent chains to halve the dependent latency.  Entries equal to m
-// have been replaced by kGone, whose terms are exactly 0.  Entries past the
+// have been replaced by a stand-in whose terms are exactly 0.  Entries past the
 // row end are -inf and only occur in a row's last chunk (TAIL), where t is
 // clamped so that e * t stays 0.
 template <bool TAIL>
@@ -210,7 +207,10 @@ struct ChunkRed {
 };
 
 // Sets aside this thread's entries equal to the chunk maximum m: counts
-// them, keeps their two lowest indices and replaces them by kGone.  Only
+// them, keeps their two lowest indices and replaces them by a stand-in value
+// far enough below m that its exponential is exactly 0 and its product with
+// the scaled difference stays finite (m - |m|/16 - 256, with the lowest
+// mantissa bit set so that it is no bfloat16 value and no input equals it).  Only
 // groups where some lane holds m are visited (usually one group of one lane
 // per chunk; the test is wave-uniform), in descending order so that the
 // lowest index is assigned last.  For draft rows a group's maximum that
@@ -224,6 +224,7 @@ __device__ __forceinline__ void set_aside_max(float (&x)[kE], float (&gm)[kU], f
   for (int u = kU - 1; u >= 0; --u) {
     if (__any(gm[u] == m)) {
       hit = true;
+      const float gone = __int_as_float(__float_as_int(m - (fabsf(m) * 0.0625f + 256.f)) | 1);
       float* y = x + 8 * u;
       float t1 = kNegInf, t2 = kNegInf;  // t1 >= t2: the group's two largest values
 #pragma unroll
@@ -236,7 +237,7 @@ __device__ __forceinline__ void set_aside_max(float (&x)[kE], float (&gm)[kU], f
         cnt += eq ? 1 : 0;
         f2 = eq ? f1 : f2;
         f1 = eq ? entry_index(v0, 8 * u + j) : f1;
-        y[j] = eq ? kGone : y[j];
+        y[j] = eq ? gone : y[j];
       }
       if (DRAFT && gm[u] == m) gm[u] = t2;
     }

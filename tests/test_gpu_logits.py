@@ -22,7 +22,7 @@ RTOL = 1e-4
 def rel_ok(got, want, rtol=RTOL, floor=0.0):
     got = np.asarray(got, dtype=np.float64)
     want = np.asarray(want, dtype=np.float64)
-    bad = np.abs(got - want) > rtol * np.abs(want) + floor
+    bad = ~(np.abs(got - want) <= rtol * np.abs(want) + floor)  # NaN counts as a mismatch
     assert not bad.any(), f"{bad.sum()} mismatches, worst got {got[bad][:3]} want {want[bad][:3]}"
 
 
@@ -98,6 +98,32 @@ def test_vocab_sizes_and_tails(vocab):
     rp = torch.tensor([0, 4, 4, 9], dtype=torch.int32, device=DEV)
     tok = torch.argmax(logits.float(), dim=1).to(torch.int32)
     tok[6] = (tok[6] + 1) % vocab
+    res = binding.verify_accept(logits, rp, tok)
+    torch.cuda.synchronize()
+    check_verify(logits, rp.cpu().numpy(), tok, res)
+
+
+def test_masked_vocabulary_entries():
+    """Most of each row masked to -1e30 (a finite mask value, as samplers
+    write them): the masked entries carry no probability and the statistics
+    are those of the unmasked ones; a row with a single unmasked entry has
+    p1 = 1 and entropy 0, and the runner-up is the first masked index."""
+    g = torch.Generator(device=DEV).manual_seed(11)
+    vocab = 40000
+    x = torch.randn(8, vocab, generator=g, device=DEV) * 2
+    keep = torch.rand(8, vocab, generator=g, device=DEV) < 0.1
+    keep[:, 0] = True
+    keep[5] = False
+    keep[5, 123] = True                  # one unmasked entry
+    keep[6] = False
+    keep[6, 7] = True
+    keep[6, 39999] = True                # two, in different chunks
+    x = torch.where(keep, x, torch.full_like(x, -1e30))
+    logits = x.to(torch.bfloat16)
+    check_draft(logits, run_draft(logits))
+    rp = torch.tensor([0, 3, 8], dtype=torch.int32, device=DEV)
+    tok = torch.argmax(logits.float(), dim=1).to(torch.int32)
+    tok[1] = (tok[1] + 1) % vocab
     res = binding.verify_accept(logits, rp, tok)
     torch.cuda.synchronize()
     check_verify(logits, rp.cpu().numpy(), tok, res)
