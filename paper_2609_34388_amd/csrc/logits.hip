@@ -113,23 +113,6 @@ __device__ __forceinline__ void load_chunk(const uint16_t* row, int v0, int v1, 
   }
 }
 
-// Wave reductions: four DPP steps (xor 1, xor 2, half-row mirror, row
-// mirror) leave every lane of a 16-lane row holding that row's result; the
-// four row results are then read as scalars and combined, so every lane gets
-// the wave's result without going through LDS.
-template <int CTRL>
-__device__ __forceinline__ int dpp(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
-}
-template <int CTRL>
-__device__ __forceinline__ float dpp(float v) {
-  return __int_as_float(dpp<CTRL>(__float_as_int(v)));
-}
-constexpr int kDppXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
-constexpr int kDppXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
-constexpr int kDppHalfMirror = 0x141;
-constexpr int kDppMirror = 0x140;
-
 template <typename T>
 __device__ __forceinline__ T lane_read(T v, int l) {
   if constexpr (sizeof(T) == 4 && __is_same(T, float))
@@ -138,35 +121,49 @@ __device__ __forceinline__ T lane_read(T v, int l) {
     return __builtin_amdgcn_readlane(v, l);
 }
 
-template <typename T, typename Op>
-__device__ __forceinline__ T wave_reduce(T v, Op op) {
-  v = op(v, dpp<kDppXor1>(v));
-  v = op(v, dpp<kDppXor2>(v));
-  v = op(v, dpp<kDppHalfMirror>(v));
-  v = op(v, dpp<kDppMirror>(v));
-  return op(op(lane_read(v, 0), lane_read(v, 16)), op(lane_read(v, 32), lane_read(v, 48)));
+// Wave reductions, six instructions with a DPP operand, in place: xor 1,
+// xor 2, half-row mirror and row mirror leave every lane of a 16-lane row
+// holding its row's result; row_bcast:15 then combines rows 0 and 1 into row
+// 1 and rows 2 and 3 into row 3, and row_bcast:31 rows 1 and 3 into row 3,
+// so lane 63 holds the wave's result, read once as a scalar.  Each step
+// first waits the two wait states a DPP read of a just-written VGPR needs.
+// Every lane of the wave must be active.
+#define RG_WAVE_REDUCE_ASM(INSN)                                                        \
+  "s_nop 1\n " INSN " %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n" \
+  "s_nop 1\n " INSN " %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n" \
+  "s_nop 1\n " INSN " %0, %0, %0 row_half_mirror row_mask:0xf bank_mask:0xf\n"     \
+  "s_nop 1\n " INSN " %0, %0, %0 row_mirror row_mask:0xf bank_mask:0xf\n"          \
+  "s_nop 1\n " INSN " %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n"        \
+  "s_nop 1\n " INSN " %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf"
+__device__ __forceinline__ float wave_sum(float v) {
+  asm volatile(RG_WAVE_REDUCE_ASM("v_add_f32_dpp") : "+v"(v));
+  return lane_read(v, 63);
+}
+__device__ __forceinline__ float wave_max(float v) {
+  asm volatile(RG_WAVE_REDUCE_ASM("v_max_f32_dpp") : "+v"(v));
+  return lane_read(v, 63);
+}
+__device__ __forceinline__ int wave_isum(int v) {
+  asm volatile(RG_WAVE_REDUCE_ASM("v_add_u32_dpp") : "+v"(v));
+  return lane_read(v, 63);
+}
+__device__ __forceinline__ int wave_imin(int v) {
+  asm volatile(RG_WAVE_REDUCE_ASM("v_min_i32_dpp") : "+v"(v));
+  return lane_read(v, 63);
+}
+// The two smallest of the lanes' disjoint index pairs {v1 <= v2}: the
+// smallest first index, then the smallest of the other lanes' first indices
+// and that lane's second one.
+__device__ __forceinline__ void wave_min2(int& v1, int& v2) {
+  const int a1 = wave_imin(v1);
+  v2 = wave_imin(v1 == a1 ? v2 : v1);
+  v1 = a1;
 }
 
 // Smallest and second smallest of two disjoint sets {a1 <= a2}, {b1 <= b2}.
 __device__ __forceinline__ void min2_merge(int& a1, int& a2, int b1, int b2) {
   a2 = min(max(a1, b1), min(a2, b2));
   a1 = min(a1, b1);
-}
-
-template <int CTRL>
-__device__ __forceinline__ void min2_step(int& v1, int& v2) {
-  min2_merge(v1, v2, dpp<CTRL>(v1), dpp<CTRL>(v2));
-}
-
-__device__ __forceinline__ void wave_min2(int& v1, int& v2) {
-  min2_step<kDppXor1>(v1, v2);
-  min2_step<kDppXor2>(v1, v2);
-  min2_step<kDppHalfMirror>(v1, v2);
-  min2_step<kDppMirror>(v1, v2);
-  int a1 = lane_read(v1, 0), a2 = lane_read(v2, 0);
-  for (int l = 16; l < 64; l += 16) min2_merge(a1, a2, lane_read(v1, l), lane_read(v2, l));
-  v1 = a1;
-  v2 = a2;
 }
 
 // Z'' and S partial sums of this thread's entries against the chunk maximum
@@ -269,8 +266,7 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
   float a1 = gm[0];
 #pragma unroll
   for (int u = 1; u < kU; ++u) a1 = max2_of(a1, gm[u]);
-  const auto fmax2 = [](float p, float q) { return max2_of(p, q); };
-  a1 = wave_reduce(a1, fmax2);
+  a1 = wave_max(a1);
   if (lane == 0) red.m[wave] = a1;
   __syncthreads();
   m = max2_of(max2_of(red.m[0], red.m[1]), max2_of(red.m[2], red.m[3]));
@@ -286,15 +282,13 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
 #pragma unroll
     for (int u = 1; u < kU; ++u) c2 = max2_of(c2, gm[u]);
   }
-  const auto add = [](float p, float q) { return p + q; };
-  const auto imin = [](int p, int q) { return min(p, q); };
-  zz = wave_reduce(zz, add);
-  ss = wave_reduce(ss, add);
-  if (DRAFT) c2 = wave_reduce(c2, fmax2);
+  zz = wave_sum(zz);
+  ss = wave_sum(ss);
+  if (DRAFT) c2 = wave_max(c2);
   if (hit) {  // wave-uniform
-    cnt = wave_reduce(cnt, [](int p, int q) { return p + q; });
+    cnt = wave_isum(cnt);
     if (DRAFT) wave_min2(f1, f2);
-    else f1 = wave_reduce(f1, imin);
+    else f1 = wave_imin(f1);
   }
   if (lane == 0) {
     red.zs[0][wave] = zz;
@@ -322,7 +316,7 @@ __device__ __forceinline__ void chunk_state(const uint16_t* row, int v0, int v1,
             if (x[8 * u + j] == v2) g = entry_index(v0, 8 * u + j);
         }
       }
-      if (scanned) g = wave_reduce(g, imin);
+      if (scanned) g = wave_imin(g);
       if (lane == 0) red.g[wave] = g;
       __syncthreads();
       g = min(min(red.g[0], red.g[1]), min(red.g[2], red.g[3]));
