@@ -89,6 +89,38 @@ def test_peaked_rows_entropy_accuracy():
     check_draft(logits, run_draft(logits))
 
 
+def test_extremes_at_every_lane_row_and_wave():
+    """Maxima, runners-up and duplicated maxima placed in each 16-lane row of
+    each wave of a chunk's work group (thread t of the group holds entries
+    (u * 256 + t) * 8 + j of its chunk), so every step of the in-wave
+    reductions and of the merge across waves decides some row."""
+    vocab = 2 * 8192 + 100
+    lanes = [0, 15, 16, 31, 32, 47, 48, 63]
+    rows = []
+    g = torch.Generator(device="cpu").manual_seed(11)
+    for w in range(4):
+        for li, lane in enumerate(lanes):
+            for chunk in (0, 1):
+                base = torch.randn(vocab, generator=g) * 0.5
+                at = chunk * 8192 + ((li % 4) * 256 + w * 64 + lane) * 8 + (li % 8)
+                other = ((li + 1) % 4 * 256 + (w + 1) % 4 * 64 + lanes[(li + 3) % 8]) * 8 + 5
+                base[at] = 6.0
+                base[other] = 5.0  # runner-up in another wave, row and chunk
+                rows.append(base.clone())
+                dup = base.clone()
+                dup[other] = 6.0  # the maximum twice: the lower index is top-1
+                rows.append(dup)
+    logits = torch.stack(rows).to(torch.bfloat16).to(DEV)
+    check_draft(logits, run_draft(logits))
+    n = logits.shape[0]
+    rp = torch.tensor([0, n // 2, n], dtype=torch.int32, device=DEV)
+    tok = torch.argmax(logits.float(), dim=1).to(torch.int32)
+    tok[n // 2 + 7] = (tok[n // 2 + 7] + 1) % vocab
+    res = binding.verify_accept(logits, rp, tok)
+    torch.cuda.synchronize()
+    check_verify(logits, rp.cpu().numpy(), tok, res)
+
+
 @pytest.mark.parametrize("vocab", [2, 7, 1000, 8192, 8193, 16384, 16385, 128250])
 def test_vocab_sizes_and_tails(vocab):
     g = torch.Generator(device=DEV).manual_seed(vocab)
