@@ -135,6 +135,19 @@ def test_vocab_sizes_and_tails(vocab):
     check_verify(logits, rp.cpu().numpy(), tok, res)
 
 
+def test_verify_single_entry_vocabulary():
+    """rg_verify_accept accepts vocab = 1: every row's argmax is 0 and its
+    entropy 0, so a row matches exactly when its token is 0."""
+    logits = torch.tensor([[1.5], [-2.0], [0.0], [7.0], [3.0]], dtype=torch.bfloat16, device=DEV)
+    rp = torch.tensor([0, 2, 2, 5], dtype=torch.int32, device=DEV)
+    tok = torch.tensor([0, 0, 0, -1, 0], dtype=torch.int32, device=DEV)
+    res = binding.verify_accept(logits, rp, tok)
+    torch.cuda.synchronize()
+    check_verify(logits, rp.cpu().numpy(), tok, res)
+    assert res["row_argmax"].cpu().tolist() == [0] * 5
+    assert res["accept_len"].cpu().tolist() == [2, 0, 1]
+
+
 def test_masked_vocabulary_entries():
     """Most of each row masked to -1e30 (a finite mask value, as samplers
     write them): the masked entries carry no probability and the statistics
