@@ -110,6 +110,39 @@ def test_edge_cases(case):
     check(out, lse, reference(lay, inp))
 
 
+def _random_case(i):
+    """Seeded random layout i of the sweep: shapes, GQA group, head size,
+    empty and long requests, and a forced or automatic chunk size."""
+    r = np.random.default_rng(1000 + i)
+    R = int(r.integers(1, 7))
+    hkv = int(r.choice([1, 2, 8]))
+    g = int(r.choice([1, 2, 4, 8] if hkv < 8 else [1, 2, 4]))
+    D = int(r.choice([64, 128]))
+    ctx = r.integers(0, 1600, R)
+    nv = r.integers(0, 24, R)
+    nd = r.integers(0, 40, R)
+    nd[(nv + nd) == 0] = 1
+    if R > 1 and r.random() < 0.3:
+        k = int(r.integers(0, R))
+        ctx[k], nv[k], nd[k] = 0, 0, 0  # an empty request
+        if (nv + nd).sum() == 0:
+            nd[(k + 1) % R] = 1
+    chunk = str(int(r.choice([0, 128, 256, 384, 640])))
+    return dict(R=R, ctx=ctx.tolist(), nv=nv.tolist(), nd=nd.tolist(), hq=hkv * g, hkv=hkv, D=D, chunk=chunk)
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_random_layouts(monkeypatch, i):
+    case = _random_case(i)
+    if case["chunk"] != "0":
+        monkeypatch.setenv("RG_ATTN_CHUNK", case["chunk"])
+    lay = _custom(case["R"], case["ctx"], case["nv"], case["nd"], hq=case["hq"], hkv=case["hkv"], D=case["D"],
+                  seed=i)
+    inp = W.make_attention_inputs(lay, DEV, poison=float("nan"))
+    out, lse = run(lay, inp)
+    check(out, lse, reference(lay, inp))
+
+
 @pytest.mark.parametrize("chunk,expect", [("64", 128), ("128", 128), ("320", 384), ("1024", 1024)])
 def test_split_kv_chunks(monkeypatch, chunk, expect):
     monkeypatch.setenv("RG_ATTN_CHUNK", chunk)
