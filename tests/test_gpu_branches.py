@@ -107,6 +107,49 @@ def test_multibranch_attention_matches_oracle(name):
     _check(out, lse, _reference(lay, inp, branches))
 
 
+def _random_branch_case(i):
+    """Seeded random batch i: per request up to three branches of any shape,
+    or a regular family (equal rows and lead, prefixes growing by a step),
+    over random contexts, GQA groups and head sizes, with a forced or
+    automatic chunk size."""
+    r = np.random.default_rng(2000 + i)
+    R = int(r.integers(1, 5))
+    hkv = int(r.choice([1, 2, 4]))
+    g = int(r.choice([1, 2, 4]))
+    D = int(r.choice([64, 128]))
+    ctx, nv, branches = [], [], []
+    for _ in range(R):
+        v = int(r.integers(0, 12))
+        kind = r.choice(["none", "free", "family"], p=[0.2, 0.45, 0.35])
+        br = []
+        if kind == "free" or (kind == "none" and v == 0):
+            for _ in range(int(r.integers(1, 4))):
+                rows = int(r.integers(1, 20))
+                br.append((int(r.integers(0, v + 1)), int(r.integers(0, min(rows, 15) + 1)), rows))
+        elif kind == "family":
+            k, rows = int(r.integers(2, 7)), int(r.integers(1, 9))
+            lead = int(r.integers(0, min(rows, 15) + 1))
+            step = int(r.integers(0, v // (k - 1) + 1))  # prefixes p0 + j step stay within 0 .. V
+            p0 = int(r.integers(0, v - (k - 1) * step + 1))
+            br = [(p0 + j * step, lead, rows) for j in range(k)]
+        ctx.append(int(r.integers(0, 1500)))
+        nv.append(v)
+        branches.append(br)
+    chunk = str(int(r.choice([0, 128, 256, 512])))
+    return ctx, nv, branches, dict(hq=hkv * g, hkv=hkv, D=D), chunk
+
+
+@pytest.mark.parametrize("i", range(16))
+def test_random_branch_layouts(monkeypatch, i):
+    ctx, nv, branches, shape, chunk = _random_branch_case(i)
+    if chunk != "0":
+        monkeypatch.setenv("RG_ATTN_CHUNK", chunk)
+    lay = _layout(ctx, nv, branches, seed=i, **shape)
+    inp = W.make_attention_inputs(lay, DEV, poison=float("nan"))
+    out, lse = _run(lay, inp, branches)
+    _check(out, lse, _reference(lay, inp, branches))
+
+
 @pytest.mark.parametrize("name", ["overlap", "split", "gap", "quadratic"])
 def test_multibranch_one_launch_mode_matches_oracle(monkeypatch, name):
     """The branched plans in the one-launch work-queue mode (RG_ATTN_PERSIST=1),
