@@ -272,3 +272,39 @@ def test_fused_round_matches_separate_calls(case):
         _same(sd, fd)
         check_draft(inp["draft_logits"], fd)
     check_verify(inp["verify_logits"], lay.row_indptr, inp["draft_tokens"], fv)
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_random_rounds(i):
+    """Seeded random rounds through rg_verify_and_confidence: vocabulary size,
+    requests (some without verify rows), row counts, sharp or flat rows, exact
+    ties and draft tokens that match the argmax for a random prefix of each
+    request, against the oracle."""
+    r = np.random.default_rng(3000 + i)
+    vocab = int(r.choice([2, 3, 100, 4097, 8191, 8192, 20000, 65537, 128256, 151936]))
+    R = int(r.integers(1, 24))
+    nv = r.integers(0, 10, R)
+    nv[r.random(R) < 0.2] = 0
+    nd_total = int(r.integers(0, 60))
+    rows_v = int(nv.sum())
+    g = torch.Generator(device="cpu").manual_seed(i)
+    def rows(n):
+        x = torch.randn(n, vocab, generator=g) * float(r.choice([0.5, 2.0, 6.0]))
+        if n and vocab > 4:
+            k = torch.randint(0, vocab, (n,), generator=g)
+            x[torch.arange(n), k] += float(r.choice([0.0, 8.0, 30.0]))  # sharp rows
+            x[: n // 3, 1] = x[: n // 3].max(dim=1).values  # exact ties with the maximum
+        return x.to(torch.bfloat16).to(DEV)
+    vlog, dlog = rows(rows_v), rows(nd_total)
+    rp = torch.as_tensor(np.concatenate([[0], np.cumsum(nv)]).astype(np.int32), device=DEV)
+    tok = torch.argmax(vlog.float(), dim=1).to(torch.int32) if rows_v else torch.zeros(0, dtype=torch.int32, device=DEV)
+    if rows_v:
+        flip = torch.as_tensor(r.random(rows_v) < 0.3, device=DEV)
+        tok = torch.where(flip, (tok + 1) % vocab, tok)
+        tok[torch.as_tensor(r.random(rows_v) < 0.05, device=DEV)] = -1  # bonus rows
+    ws = binding.new_workspace(binding.verify_and_confidence_workspace_bytes(R, rows_v, nd_total, vocab), DEV)
+    fv, fd = binding.verify_and_confidence(vlog, rp, tok, dlog, workspace=ws)
+    torch.cuda.synchronize()
+    check_verify(vlog, rp.cpu().numpy(), tok, fv)
+    if nd_total:
+        check_draft(dlog, fd)
